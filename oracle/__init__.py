@@ -1,0 +1,7 @@
+"""Float64 CPU oracle of the encoder layer (test infrastructure only).
+
+Only the tests, the smoke check and the CPU-baseline leg of the benchmark
+import this package.  The product library never does.
+"""
+from .encoder_layer import *  # noqa: F401,F403
+from .encoder_layer import __all__  # noqa: F401
