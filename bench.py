@@ -1,0 +1,228 @@
+"""Benchmark of the encoder-layer kernel chain on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config vit22b]
+
+One step is one forward + backward pass of one encoder layer over one
+micro-batch of synthetic tokens, launched kernel by kernel through the C ABI
+(the separately schedulable units; the composite entry points run the same
+kernels and are bit-identical).  Every launch is bracketed by HIP events on
+the stream it runs on, so the timed region also yields each kernel's p50
+latency.  Prints one JSON line: fwd+bwd TFLOP/s of the whole chain (and its
+fraction of the bf16 MFMA peak), per-kernel p50 latencies, the roofline of
+the dominant kernel, and the float64 oracle timed on the host cores over a
+bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="vit22b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+class Chain:
+    """Preallocated buffers and the kernel-by-kernel layer step."""
+
+    def __init__(self, cfg, x, params, dout):
+        from paper_2408_03505_amd import binding as B
+        self.B, self.cfg, self.x, self.p, self.dout = B, cfg, x, params, dout
+        Bn, S, H, nh, d, F = (cfg[k] for k in ("batch", "seq", "hidden", "heads", "head_dim", "mlp"))
+        M, A = Bn * S, nh * d
+        dev = x.device
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        e = torch.empty
+        self.t = t = {
+            "y1": e((M, H), **bf), "mean1": e((M,), **f32), "rstd1": e((M,), **f32), "qkv": e((M, 3 * A), **bf),
+            "o": e((M, A), **bf), "lse": e((Bn, nh, S), **f32), "h": e((M, H), **bf), "y2": e((M, H), **bf),
+            "mean2": e((M,), **f32), "rstd2": e((M,), **f32), "u": e((M, F), **bf), "g": e((M, F), **bf),
+            "out": e((M, H), **bf), "du": e((M, F), **bf), "dy2": e((M, H), **bf), "dh": e((M, H), **bf),
+            "do": e((M, A), **bf), "dqkv": e((M, 3 * A), **bf), "dy1": e((M, H), **bf), "dx": e((M, H), **bf),
+        }
+        self.g = {n: torch.zeros(tuple(params[n].shape), **f32) for n in params}
+        self.ln_ws = e((B.ln_bwd_workspace_bytes(M, H),), dtype=torch.uint8, device=dev)
+        self.attn_ws = e((B.attn_bwd_workspace_bytes(Bn, S, nh, d),), dtype=torch.uint8, device=dev)
+        self.M, self.A = M, A
+        self.kernels = self._kernels()
+
+    def _kernels(self):
+        B, c, x, p, dout, t, g = self.B, self.cfg, self.x, self.p, self.dout, self.t, self.g
+        Bn, S, nh, d, eps = c["batch"], c["seq"], c["heads"], c["head_dim"], c["ln_eps"]
+        return [
+            ("ln1_fwd", lambda: B.enc_ln_fwd(x, p["ln1_g"], p["ln1_b"], eps, t["y1"], t["mean1"], t["rstd1"])),
+            ("qkv_fwd", lambda: B.enc_qkv_fwd(t["y1"], p["w_qkv"], p["b_qkv"], t["qkv"])),
+            ("attn_fwd", lambda: B.enc_attn_fwd(Bn, S, nh, d, t["qkv"], t["o"], t["lse"])),
+            ("oproj_fwd", lambda: B.enc_oproj_fwd(t["o"], p["w_o"], p["b_o"], x, t["h"])),
+            ("ln2_fwd", lambda: B.enc_ln_fwd(t["h"], p["ln2_g"], p["ln2_b"], eps, t["y2"], t["mean2"], t["rstd2"])),
+            ("mlp_up_fwd", lambda: B.enc_mlp_up_fwd(t["y2"], p["w_1"], p["b_1"], t["u"], t["g"])),
+            ("mlp_down_fwd", lambda: B.enc_mlp_down_fwd(t["g"], p["w_2"], p["b_2"], t["h"], t["out"])),
+            ("mlp_down_bwd_data", lambda: B.enc_mlp_down_bwd_data(dout, p["w_2"], t["u"], t["du"])),
+            ("mlp_down_bwd_weight", lambda: B.enc_mlp_down_bwd_weight(dout, t["g"], g["w_2"], g["b_2"])),
+            ("mlp_up_bwd_data", lambda: B.enc_mlp_up_bwd_data(t["du"], p["w_1"], t["dy2"])),
+            ("mlp_up_bwd_weight", lambda: B.enc_mlp_up_bwd_weight(t["du"], t["y2"], g["w_1"], g["b_1"])),
+            ("ln2_bwd", lambda: B.enc_ln_bwd(t["dy2"], t["h"], t["mean2"], t["rstd2"], p["ln2_g"], dout, t["dh"],
+                                             g["ln2_g"], g["ln2_b"], ws=self.ln_ws)),
+            ("oproj_bwd_data", lambda: B.enc_oproj_bwd_data(t["dh"], p["w_o"], t["do"])),
+            ("oproj_bwd_weight", lambda: B.enc_oproj_bwd_weight(t["dh"], t["o"], g["w_o"], g["b_o"])),
+            ("attn_bwd", lambda: B.enc_attn_bwd(Bn, S, nh, d, t["qkv"], t["o"], t["lse"], t["do"], t["dqkv"],
+                                                ws=self.attn_ws)),
+            ("qkv_bwd_data", lambda: B.enc_qkv_bwd_data(t["dqkv"], p["w_qkv"], t["dy1"])),
+            ("qkv_bwd_weight", lambda: B.enc_qkv_bwd_weight(t["dqkv"], t["y1"], g["w_qkv"], g["b_qkv"])),
+            ("ln1_bwd", lambda: B.enc_ln_bwd(t["dy1"], x, t["mean1"], t["rstd1"], p["ln1_g"], t["dh"], t["dx"],
+                                             g["ln1_g"], g["ln1_b"], ws=self.ln_ws)),
+        ]
+
+
+def kernel_work(cfg):
+    """Algorithmic work of each kernel: (flops, bytes)."""
+    Bn, S, H, nh, d, F = (cfg[k] for k in ("batch", "seq", "hidden", "heads", "head_dim", "mlp"))
+    M, A = Bn * S, nh * d
+    att = 4 * Bn * nh * S * S * d
+    ln_f = 4 * M * H + 8 * M + 4 * H
+    ln_b = 8 * M * H + 8 * M + 2 * H + 8 * H
+    gemm = lambda m, n, k: 2 * m * n * k  # noqa: E731
+    return {
+        "ln1_fwd": (0, ln_f), "qkv_fwd": (gemm(M, 3 * A, H), 2 * (M * H + 3 * A * H + M * 3 * A)),
+        "attn_fwd": (att, 2 * (3 * M * A + M * A) + 4 * Bn * nh * S),
+        "oproj_fwd": (gemm(M, H, A), 2 * (M * A + H * A + 2 * M * H)), "ln2_fwd": (0, ln_f),
+        "mlp_up_fwd": (gemm(M, F, H), 2 * (M * H + F * H + 2 * M * F)),
+        "mlp_down_fwd": (gemm(M, H, F), 2 * (M * F + H * F + 2 * M * H)),
+        "mlp_down_bwd_data": (gemm(M, F, H), 2 * (M * H + H * F + 2 * M * F)),
+        "mlp_down_bwd_weight": (gemm(H, F, M), 2 * (M * H + M * F) + 4 * (H * F + H)),
+        "mlp_up_bwd_data": (gemm(M, H, F), 2 * (M * F + F * H + M * H)),
+        "mlp_up_bwd_weight": (gemm(F, H, M), 2 * (M * F + M * H) + 4 * (F * H + F)),
+        "ln2_bwd": (0, ln_b), "oproj_bwd_data": (gemm(M, A, H), 2 * (M * H + H * A + M * A)),
+        "oproj_bwd_weight": (gemm(H, A, M), 2 * (M * H + M * A) + 4 * (H * A + H)),
+        "attn_bwd": (2 * att, 2 * (3 * M * A + 2 * M * A + 3 * M * A) + 4 * Bn * nh * S),
+        "qkv_bwd_data": (gemm(M, H, 3 * A), 2 * (M * 3 * A + 3 * A * H + M * H)),
+        "qkv_bwd_weight": (gemm(3 * A, H, M), 2 * (M * 3 * A + M * H) + 4 * (3 * A * H + 3 * A)),
+        "ln1_bwd": (0, ln_b),
+    }
+
+
+def cpu_baseline(cfg, x, params, dout, budget_s):
+    """The float64 oracle's layer forward+backward on whole sequences of the
+    same workload (as many as fit the time budget, at least one)."""
+    import oracle
+    from threadpoolctl import threadpool_info
+
+    S, H = cfg["seq"], cfg["hidden"]
+    p64 = {n: params[n].to(torch.float64).numpy() for n in params}
+    done, t_used, flops = 0, 0.0, 0
+    one = dict(cfg, batch=1)
+    f1 = 3 * oracle.layer_flops(one)
+    while done < cfg["batch"]:
+        xs = x[done * S:(done + 1) * S].to(torch.float64).numpy()
+        ds = dout[done * S:(done + 1) * S].to(torch.float64).numpy()
+        t0 = time.perf_counter()
+        out, saved = oracle.layer_fwd(one, p64, xs)
+        oracle.layer_bwd(one, p64, xs, saved, ds)
+        t_used += time.perf_counter() - t0
+        done += 1
+        flops += f1
+        if t_used + t_used / done > budget_s:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": flops / t_used / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle forward+backward of {done} of {cfg['batch']} sequences "
+                      f"({done * S} tokens) of the same layer, {t_used:.1f} s",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are out of scope "
+                                   "(--gpus must be 1)"}), flush=True)
+        sys.exit(2)
+    from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs
+    import oracle
+
+    cfg = CONFIGS[args.config]
+    x, params, dout = layer_inputs(cfg, seed=args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gx, gd = x.to(dev), dout.to(dev)
+    gp = {n: params[n].to(dev) for n in params}
+    chain = Chain(cfg, gx, gp, gd)
+    names = [n for n, _ in chain.kernels]
+    K, W = args.steps, args.warmup
+
+    for _ in range(W):
+        for _, fn in chain.kernels:
+            fn()
+    torch.cuda.synchronize()
+
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in names]
+          for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        for i, (_, fn) in enumerate(chain.kernels):
+            ev[k][i][0].record()
+            fn()
+            ev[k][i][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    per = {n: [ev[k][i][0].elapsed_time(ev[k][i][1]) * 1e3 for k in range(K)] for i, n in enumerate(names)}
+    p50 = {n: float(np.median(v)) for n, v in per.items()}
+    avg = {n: float(np.mean(v)) for n, v in per.items()}
+    work = kernel_work(cfg)
+    flops_step = 3 * oracle.layer_flops(cfg)
+    assert abs(sum(w[0] for w in work.values()) - flops_step) < 1e-6 * flops_step
+    ms = wall / K * 1e3
+    tflops = flops_step / (wall / K) / 1e12
+
+    dom = max(names, key=lambda n: avg[n])
+    dflops = work[dom][0]
+    achieved = dflops / (avg[dom] * 1e-6) / 1e12
+    per_kernel = {n: {"p50_us": round(p50[n], 2),
+                      "tflops": round(work[n][0] / (p50[n] * 1e-6) / 1e12, 1) if work[n][0] else None,
+                      "gbs": round(work[n][1] / (p50[n] * 1e-6) / 1e9, 1),
+                      "frac": round((work[n][0] / (p50[n] * 1e-6) / 1e12) / PEAK_BF16_TFLOPS, 3) if work[n][0]
+                      else round(work[n][1] / (p50[n] * 1e-6) / 1e9 / PEAK_HBM_GBS, 3)} for n in names}
+
+    res = {
+        "metric": "encoder layer fwd+bwd TFLOPS (% bf16 MFMA peak) + per-kernel p50 latency (us)",
+        "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{args.config} encoder layer fwd+bwd", **{k: cfg[k] for k in (
+            "batch", "seq", "hidden", "heads", "head_dim", "mlp")}},
+        "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "sum_kernel_p50_ms": round(sum(p50.values()) / 1e3, 4),
+        "max_kernel_p50_us": round(max(p50.values()), 2),
+        "per_kernel": per_kernel,
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "avg_launch_us": round(avg[dom], 2)},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, x, params, dout, args.cpu_budget_s)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,264 @@
+/*
+ * optimus_enc.h - C ABI of the fine-grained ViT encoder-layer kernels.
+ *
+ * Optimus (arXiv 2408.03505) trains multimodal LLMs by running vision-encoder
+ * work inside the LLM pipeline's idle periods.  Many of those bubbles last
+ * well under a millisecond (about 300 us for tensor-parallel bubbles, §2.3,
+ * challenge 3), shorter than one encoder layer's forward or backward, so the
+ * paper decomposes the encoder layer into a series of kernels and schedules
+ * those kernels individually (abstract; §3.1, design decision 3; §4.2, the
+ * ScheduleKernels step, which packs kernels into a bubble while their summed
+ * time fits and keeps the encoder's internal order).  Forward and backward are
+ * scheduled separately, and the backward may be skipped for a frozen encoder
+ * (§6, frozen parameters).
+ *
+ * This library provides that chain for one pre-LN ViT layer on one
+ * micro-batch: a composite forward and backward plus one entry point per
+ * kernel, each of which only enqueues work on a caller-given HIP stream.
+ * Parameters and activations are bfloat16; parameter gradients are fp32
+ * (bf16 parameters with fp32 gradients, §4.5 memory analysis).
+ *
+ * Conventions shared by every entry point
+ *  - enc_bf16 is bfloat16 storage (round-to-nearest-even from fp32).
+ *  - Every tensor is dense and row-major.  Token rows M = batch*seq are
+ *    ordered sequence-major (row r = b*seq + s).  Weights are [out, in].
+ *    qkv columns are packed [3][heads][head_dim]; attention outputs are
+ *    packed [heads][head_dim].
+ *  - Every pointer is a DEVICE pointer owned by the caller.  The library never
+ *    allocates, frees or synchronises, and keeps no global mutable state
+ *    besides a thread-local last-error string.  Inputs are never written.
+ *    Outputs must not alias inputs, except that with accumulate=1 the fp32
+ *    gradient buffers are read and written.
+ *  - Every tensor pointer must be 16-byte aligned.  hidden, heads*head_dim and
+ *    mlp must be multiples of 8; head_dim must be 64, 80 or 128.
+ *  - Each call validates its arguments, enqueues its kernels on `stream`
+ *    (a hipStream_t; NULL is the null stream) and returns.  Device faults
+ *    surface at the caller's next synchronisation.  Calls contain no host
+ *    synchronisation and no allocation, so they can be captured into HIP
+ *    graphs.
+ *  - Return value: ENC_OK (0) or a negative enc_status; enc_last_error()
+ *    then describes the failure.  On error nothing has been enqueued, except
+ *    for ENC_ERR_LAUNCH, which reports a failed launch after earlier kernels
+ *    of the same call may already have been enqueued.
+ */
+#ifndef OPTIMUS_ENC_H
+#define OPTIMUS_ENC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t enc_bf16;
+typedef void *enc_stream_t; /* hipStream_t */
+
+enum enc_status {
+  ENC_OK = 0,
+  ENC_ERR_INVALID = -1,     /* null pointer or non-positive dimension */
+  ENC_ERR_UNSUPPORTED = -2, /* shape outside what the kernels support */
+  ENC_ERR_ALIGN = -3,       /* a pointer is not 16-byte aligned */
+  ENC_ERR_LAUNCH = -4,      /* a HIP kernel launch failed */
+  ENC_ERR_WORKSPACE = -5    /* workspace smaller than the size query returned */
+};
+
+/* Shape of one encoder layer on one micro-batch.  heads*head_dim may differ
+ * from hidden: one tensor-parallel rank keeps the full LayerNorm width but
+ * only heads/TP heads and mlp/TP of the MLP.  Widths follow the ViT table
+ * of Appendix A (width, MLP dimension, heads, head dimension). */
+typedef struct {
+  int batch;    /* sequences in the micro-batch */
+  int seq;      /* tokens per sequence (patches + class token) */
+  int hidden;   /* model width H */
+  int heads;    /* attention heads on this GPU */
+  int head_dim; /* 64, 80 or 128 */
+  int mlp;      /* MLP width F on this GPU */
+  float ln_eps; /* LayerNorm epsilon, added to the variance */
+} enc_cfg_t;
+
+/* The twelve bf16 parameters (A = heads*head_dim). */
+typedef struct {
+  const enc_bf16 *ln1_g, *ln1_b; /* [H] */
+  const enc_bf16 *w_qkv;         /* [3A, H] */
+  const enc_bf16 *b_qkv;         /* [3A] */
+  const enc_bf16 *w_o;           /* [H, A] */
+  const enc_bf16 *b_o;           /* [H] */
+  const enc_bf16 *ln2_g, *ln2_b; /* [H] */
+  const enc_bf16 *w_1;           /* [F, H] */
+  const enc_bf16 *b_1;           /* [F] */
+  const enc_bf16 *w_2;           /* [H, F] */
+  const enc_bf16 *b_2;           /* [H] */
+} enc_params_t;
+
+/* fp32 parameter gradients, same shapes as enc_params_t. */
+typedef struct {
+  float *ln1_g, *ln1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+  float *ln2_g, *ln2_b, *w_1, *b_1, *w_2, *b_2;
+} enc_grads_t;
+
+/* Byte offsets of the saved-for-backward tensors inside one caller buffer
+ * (every offset is a multiple of 256).  bf16: y1, h, y2 [M,H]; qkv [M,3A];
+ * o [M,A]; u, g [M,F].  fp32: mean1, rstd1, mean2, rstd2 [M];
+ * lse [batch, heads, seq]. */
+typedef struct {
+  size_t y1, mean1, rstd1, qkv, o, lse, h, y2, mean2, rstd2, u, g;
+  size_t total; /* bytes the saved buffer must hold */
+} enc_saved_layout_t;
+
+/* ------------------------------------------------------------ status */
+
+/* Static text for a status code. */
+const char *enc_status_string(int status);
+/* Description of the last failure on the calling thread ("" if none). */
+const char *enc_last_error(void);
+/* ABI version of this header (bumped on incompatible change). */
+int enc_abi_version(void);
+
+/* ------------------------------------------------------------ sizing */
+
+/* Validates cfg and fills the saved-buffer layout. */
+int enc_saved_layout(const enc_cfg_t *cfg, enc_saved_layout_t *layout);
+/* Workspace bytes that encoder_layer_fwd / encoder_layer_bwd need. */
+int enc_layer_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes);
+/* Workspace of the per-kernel entry points that take one. */
+int enc_ln_bwd_workspace_bytes(int rows, int cols, size_t *bytes);
+int enc_attn_bwd_workspace_bytes(int batch, int seq, int heads, int head_dim, size_t *bytes);
+
+/* ------------------------------------------------------------ composites */
+
+/* Forward of one pre-LN encoder layer on one micro-batch: the kernels of
+ * the forward chain in order (LN1, QKV projection, attention, output
+ * projection + residual, LN2, MLP up + GELU, MLP down + residual) on one
+ * stream.  x, out: [M, H].  saved: enc_saved_layout().total bytes, filled
+ * with the intermediates the backward needs.  ws: workspace of
+ * enc_layer_workspace_bytes() bytes (ws_bytes states its size). */
+int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params,
+                      const enc_bf16 *x, enc_bf16 *out, void *saved,
+                      void *ws, size_t ws_bytes, enc_stream_t stream);
+
+/* Backward of encoder_layer_fwd given dout = dL/dout [M, H]: writes
+ * dx [M, H] and the twelve parameter gradients (overwritten when
+ * accumulate=0, added to when accumulate=1).  saved is the buffer the
+ * forward filled for the same x and params. */
+int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params,
+                      const enc_bf16 *x, const void *saved,
+                      const enc_bf16 *dout, enc_bf16 *dx,
+                      const enc_grads_t *grads, int accumulate,
+                      void *ws, size_t ws_bytes, enc_stream_t stream);
+
+/* ------------------------------------------------------------ forward kernels */
+
+/* LayerNorm over each of `rows` rows of `cols` values: per row the mean and
+ * biased variance, rstd = 1/sqrt(var + eps), y = (x - mean)*rstd*gamma + beta.
+ * x, y: [rows, cols] bf16; gamma, beta: [cols] bf16; mean, rstd: [rows] fp32
+ * (kept for the backward).  cols must be a multiple of 8 and <= 16384. */
+int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma,
+               const enc_bf16 *beta, float eps, enc_bf16 *y, float *mean,
+               float *rstd, enc_stream_t stream);
+
+/* QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A]. */
+int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv,
+                const enc_bf16 *b_qkv, enc_bf16 *qkv, enc_stream_t stream);
+
+/* Bidirectional softmax attention of every (sequence, head): for queries i
+ * and keys j of one sequence, P = softmax_j(q_i . k_j / sqrt(head_dim)),
+ * o_i = sum_j P_ij v_j.  qkv: [batch*seq, 3*heads*head_dim] as written by
+ * enc_qkv_fwd; o: [batch*seq, heads*head_dim]; lse: [batch, heads, seq] fp32,
+ * the natural-log normaliser log sum_j exp(q_i . k_j / sqrt(head_dim)). */
+int enc_attn_fwd(int batch, int seq, int heads, int head_dim,
+                 const enc_bf16 *qkv, enc_bf16 *o, float *lse,
+                 enc_stream_t stream);
+
+/* Output projection with residual: h[M, H] = resid[M, H] + o[M, A] *
+ * w_o[H, A]^T + b_o[H]. */
+int enc_oproj_fwd(int M, int A, int H, const enc_bf16 *o, const enc_bf16 *w_o,
+                  const enc_bf16 *b_o, const enc_bf16 *resid, enc_bf16 *h,
+                  enc_stream_t stream);
+
+/* MLP up-projection with GELU: u[M, F] = y2[M, H] * w_1[F, H]^T + b_1[F];
+ * g = GELU(u) = u * Phi(u) (exact erf form).  Both u and g are written
+ * (u is kept for the backward). */
+int enc_mlp_up_fwd(int M, int H, int F, const enc_bf16 *y2, const enc_bf16 *w_1,
+                   const enc_bf16 *b_1, enc_bf16 *u, enc_bf16 *g,
+                   enc_stream_t stream);
+
+/* MLP down-projection with residual: out[M, H] = resid[M, H] + g[M, F] *
+ * w_2[H, F]^T + b_2[H]. */
+int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2,
+                     const enc_bf16 *b_2, const enc_bf16 *resid, enc_bf16 *out,
+                     enc_stream_t stream);
+
+/* ------------------------------------------------------------ backward kernels */
+
+/* MLP down input gradient through GELU: du[M, F] = (dout[M, H] * w_2[H, F])
+ * * GELU'(u), GELU'(u) = Phi(u) + u*phi(u); u is the saved pre-activation. */
+int enc_mlp_down_bwd_data(int M, int F, int H, const enc_bf16 *dout,
+                          const enc_bf16 *w_2, const enc_bf16 *u, enc_bf16 *du,
+                          enc_stream_t stream);
+
+/* MLP up input gradient: dy2[M, H] = du[M, F] * w_1[F, H]. */
+int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du,
+                        const enc_bf16 *w_1, enc_bf16 *dy2, enc_stream_t stream);
+
+/* Output projection input gradient: do_[M, A] = dh[M, H] * w_o[H, A]. */
+int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh,
+                       const enc_bf16 *w_o, enc_bf16 *do_, enc_stream_t stream);
+
+/* QKV projection input gradient: dy1[M, H] = dqkv[M, 3A] * w_qkv[3A, H]. */
+int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv,
+                     const enc_bf16 *w_qkv, enc_bf16 *dy1, enc_stream_t stream);
+
+/* Parameter gradients of a linear layer Y = X W^T + b, summed over the M
+ * token rows: dW[N, K] = dY[M, N]^T * X[M, K]; db[N] = sum_m dY[m, :]
+ * (db may be NULL).  fp32 outputs are overwritten (accumulate=0) or added
+ * to (accumulate=1).  The sums are deterministic (no atomics). */
+int enc_linear_bwd_weight(int M, int N, int K, const enc_bf16 *dY,
+                          const enc_bf16 *X, float *dW, float *db,
+                          int accumulate, enc_stream_t stream);
+/* The four uses of enc_linear_bwd_weight in the layer, by name:
+ *  MLP down: dw_2[H, F] = dout^T g,   db_2[H]
+ *  MLP up:   dw_1[F, H] = du^T y2,    db_1[F]
+ *  out proj: dw_o[H, A] = dh^T o,     db_o[H]
+ *  QKV:      dw_qkv[3A, H] = dqkv^T y1, db_qkv[3A] */
+int enc_mlp_down_bwd_weight(int M, int F, int H, const enc_bf16 *dout,
+                            const enc_bf16 *g, float *dw_2, float *db_2,
+                            int accumulate, enc_stream_t stream);
+int enc_mlp_up_bwd_weight(int M, int H, int F, const enc_bf16 *du,
+                          const enc_bf16 *y2, float *dw_1, float *db_1,
+                          int accumulate, enc_stream_t stream);
+int enc_oproj_bwd_weight(int M, int A, int H, const enc_bf16 *dh,
+                         const enc_bf16 *o, float *dw_o, float *db_o,
+                         int accumulate, enc_stream_t stream);
+int enc_qkv_bwd_weight(int M, int H, int A, const enc_bf16 *dqkv,
+                       const enc_bf16 *y1, float *dw_qkv, float *db_qkv,
+                       int accumulate, enc_stream_t stream);
+
+/* LayerNorm backward (exact gradient of enc_ln_fwd) with the residual
+ * branch added: with xhat = (x - mean)*rstd and ghat = dy*gamma, per row
+ * dx = dresid + rstd*(ghat - mean(ghat) - xhat*mean(ghat*xhat)); and over
+ * all rows dgamma = sum dy*xhat, dbeta = sum dy (fp32, overwritten or
+ * accumulated).  dresid may be NULL (treated as zero).  The column sums use
+ * a fixed-order two-pass reduction through ws
+ * (enc_ln_bwd_workspace_bytes). */
+int enc_ln_bwd(int rows, int cols, const enc_bf16 *dy, const enc_bf16 *x,
+               const float *mean, const float *rstd, const enc_bf16 *gamma,
+               const enc_bf16 *dresid, enc_bf16 *dx, float *dgamma,
+               float *dbeta, int accumulate, void *ws, size_t ws_bytes,
+               enc_stream_t stream);
+
+/* Attention backward (exact gradient of enc_attn_fwd): with P recomputed
+ * from lse, D_i = sum_e do_ie*o_ie, dV = P^T dO, dP = dO V^T,
+ * dS = P*(dP - D), dQ = dS K/sqrt(d), dK = dS^T Q/sqrt(d), written to
+ * dqkv [batch*seq, 3*heads*head_dim] in the qkv packing.  ws holds D
+ * (enc_attn_bwd_workspace_bytes); no atomics, deterministic. */
+int enc_attn_bwd(int batch, int seq, int heads, int head_dim,
+                 const enc_bf16 *qkv, const enc_bf16 *o, const float *lse,
+                 const enc_bf16 *do_, enc_bf16 *dqkv, void *ws,
+                 size_t ws_bytes, enc_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPTIMUS_ENC_H */

@@ -1,0 +1,559 @@
+// C-ABI entry points: argument validation, workspace/saved-buffer layout,
+// and the forward/backward chains of one encoder layer on one stream.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/optimus_enc.h"
+#include "kernels.hpp"
+
+using namespace optimus;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return ENC_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline hipStream_t as_stream(enc_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Null and alignment checks for a list of required pointers.
+struct PtrCheck {
+  int code = ENC_OK;
+  const char *fn;
+  explicit PtrCheck(const char *f) : fn(f) {}
+  PtrCheck &req(const void *p, const char *name) {
+    if (code != ENC_OK) return *this;
+    if (!p) code = fail(ENC_ERR_INVALID, "%s: %s is NULL", fn, name);
+    else if (!aligned16(p)) code = fail(ENC_ERR_ALIGN, "%s: %s is not 16-byte aligned", fn, name);
+    return *this;
+  }
+  PtrCheck &opt(const void *p, const char *name) {
+    if (code != ENC_OK || !p) return *this;
+    if (!aligned16(p)) code = fail(ENC_ERR_ALIGN, "%s: %s is not 16-byte aligned", fn, name);
+    return *this;
+  }
+};
+
+int check_dims(const char *fn, std::initializer_list<int> dims) {
+  for (int d : dims)
+    if (d <= 0) return fail(ENC_ERR_INVALID, "%s: dimensions must be positive", fn);
+  return ENC_OK;
+}
+
+int check_mult8(const char *fn, std::initializer_list<int> dims) {
+  for (int d : dims)
+    if (d % 8 != 0) return fail(ENC_ERR_UNSUPPORTED, "%s: feature widths must be multiples of 8 (got %d)", fn, d);
+  return ENC_OK;
+}
+
+// Largest product of dimensions that still indexes safely with 32-bit ints
+// inside the kernels (row index * leading dimension is computed in 64 bits,
+// but tile indices and row counts are 32-bit).
+constexpr long kMaxElems = 1L << 31;
+
+int launched(const char *fn) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(ENC_ERR_LAUNCH, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+int check_cfg(const char *fn, const enc_cfg_t *c) {
+  if (!c) return fail(ENC_ERR_INVALID, "%s: cfg is NULL", fn);
+  int r = check_dims(fn, {c->batch, c->seq, c->hidden, c->heads, c->head_dim, c->mlp});
+  if (r) return r;
+  if (c->head_dim != 64 && c->head_dim != 80 && c->head_dim != 128)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: head_dim must be 64, 80 or 128 (got %d)", fn, c->head_dim);
+  if ((r = check_mult8(fn, {c->hidden, c->heads * c->head_dim, c->mlp}))) return r;
+  if (c->hidden > 16384) return fail(ENC_ERR_UNSUPPORTED, "%s: hidden must be <= 16384", fn);
+  if (!(c->ln_eps >= 0.f)) return fail(ENC_ERR_INVALID, "%s: ln_eps must be >= 0", fn);
+  const long M = static_cast<long>(c->batch) * c->seq;
+  const long A = static_cast<long>(c->heads) * c->head_dim;
+  if (M * c->mlp >= kMaxElems || M * 3 * A >= kMaxElems || M * c->hidden >= kMaxElems ||
+      static_cast<long>(c->mlp) * c->hidden >= kMaxElems)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: a tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+void saved_layout(const enc_cfg_t *c, enc_saved_layout_t *L) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  const size_t H = c->hidden, A = static_cast<size_t>(c->heads) * c->head_dim, F = c->mlp;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  };
+  L->y1 = take(M * H * 2);
+  L->mean1 = take(M * 4);
+  L->rstd1 = take(M * 4);
+  L->qkv = take(M * 3 * A * 2);
+  L->o = take(M * A * 2);
+  L->lse = take(static_cast<size_t>(c->batch) * c->heads * c->seq * 4);
+  L->h = take(M * H * 2);
+  L->y2 = take(M * H * 2);
+  L->mean2 = take(M * 4);
+  L->rstd2 = take(M * 4);
+  L->u = take(M * F * 2);
+  L->g = take(M * F * 2);
+  L->total = off;
+}
+
+// Backward workspace regions (offsets in bytes).
+struct BwdWs {
+  size_t du, dy2, dh, dO, dqkv, dy1, ln_part, dvec, total;
+};
+
+BwdWs bwd_layout(const enc_cfg_t *c) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  const size_t H = c->hidden, A = static_cast<size_t>(c->heads) * c->head_dim, F = c->mlp;
+  BwdWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  };
+  w.du = take(M * F * 2);
+  w.dy2 = take(M * H * 2);
+  w.dh = take(M * H * 2);
+  w.dO = take(M * A * 2);
+  w.dqkv = take(M * 3 * A * 2);
+  w.dy1 = take(M * H * 2);
+  w.ln_part = take(ln_bwd_ws_bytes(static_cast<int>(M), c->hidden));
+  w.dvec = take(attn_bwd_ws_bytes(c->batch, c->seq, c->heads));
+  w.total = off;
+  return w;
+}
+
+template <class T>
+T *at(void *base, size_t off) {
+  return reinterpret_cast<T *>(static_cast<char *>(base) + off);
+}
+template <class T>
+const T *at(const void *base, size_t off) {
+  return reinterpret_cast<const T *>(static_cast<const char *>(base) + off);
+}
+
+int check_params(const char *fn, const enc_params_t *p) {
+  if (!p) return fail(ENC_ERR_INVALID, "%s: params is NULL", fn);
+  PtrCheck c(fn);
+  c.req(p->ln1_g, "ln1_g").req(p->ln1_b, "ln1_b").req(p->w_qkv, "w_qkv").req(p->b_qkv, "b_qkv");
+  c.req(p->w_o, "w_o").req(p->b_o, "b_o").req(p->ln2_g, "ln2_g").req(p->ln2_b, "ln2_b");
+  c.req(p->w_1, "w_1").req(p->b_1, "b_1").req(p->w_2, "w_2").req(p->b_2, "b_2");
+  return c.code;
+}
+
+int check_grads(const char *fn, const enc_grads_t *g) {
+  if (!g) return fail(ENC_ERR_INVALID, "%s: grads is NULL", fn);
+  PtrCheck c(fn);
+  c.req(g->ln1_g, "dln1_g").req(g->ln1_b, "dln1_b").req(g->w_qkv, "dw_qkv").req(g->b_qkv, "db_qkv");
+  c.req(g->w_o, "dw_o").req(g->b_o, "db_o").req(g->ln2_g, "dln2_g").req(g->ln2_b, "dln2_b");
+  c.req(g->w_1, "dw_1").req(g->b_1, "db_1").req(g->w_2, "dw_2").req(g->b_2, "db_2");
+  return c.code;
+}
+
+// ---- unchecked launch helpers shared by the per-kernel entry points and the chains
+
+bool gemm_fwd(int M, int N, int K, const bf16_t *X, const bf16_t *W, const bf16_t *bias, const bf16_t *R, bf16_t *Y,
+              bf16_t *Y2, Epi epi, hipStream_t s) {
+  GemmArgs a{};
+  a.M = M, a.N = N, a.K = K;
+  a.A = X, a.lda = K, a.B = W, a.ldb = K;
+  a.Y = Y, a.ldy = N, a.bias = bias, a.R = R, a.Y2 = Y2;
+  return launch_gemm_fwd(a, epi, s);
+}
+
+// dX[M, K] = dY[M, N] * W[N, K]  (optionally times GELU'(U[M, K]))
+bool gemm_dgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *U, bf16_t *dX, hipStream_t s) {
+  GemmArgs a{};
+  a.M = M, a.N = K, a.K = N;
+  a.A = dY, a.lda = N, a.B = W, a.ldb = K;
+  a.Y = dX, a.ldy = K, a.R = U;
+  return launch_gemm_dgrad(a, U ? Epi::kGeluGrad : Epi::kPlain, s);
+}
+
+// dW[N, K] (+)= dY[M, N]^T X[M, K]; db[N] (+)= sum_m dY
+bool gemm_wgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *X, float *dW, float *db, int acc, hipStream_t s) {
+  GemmArgs a{};
+  a.M = N, a.N = K, a.K = M;
+  a.A = dY, a.lda = N, a.B = X, a.ldb = K;
+  a.Wf = dW, a.ldy = K, a.db = db, a.accumulate = acc;
+  return launch_gemm_wgrad(a, s);
+}
+
+int linear_dims(const char *fn, int M, std::initializer_list<int> feats) {
+  int r = check_dims(fn, {M});
+  if (r) return r;
+  for (int f : feats)
+    if (f <= 0) return fail(ENC_ERR_INVALID, "%s: dimensions must be positive", fn);
+  for (int f : feats)
+    if (f % 8) return fail(ENC_ERR_UNSUPPORTED, "%s: feature widths must be multiples of 8 (got %d)", fn, f);
+  for (int f : feats)
+    if (static_cast<long>(M) * f >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+int attn_dims(const char *fn, int B, int S, int heads, int d) {
+  int r = check_dims(fn, {B, S, heads, d});
+  if (r) return r;
+  if (d != 64 && d != 80 && d != 128) return fail(ENC_ERR_UNSUPPORTED, "%s: head_dim must be 64, 80 or 128", fn);
+  if (static_cast<long>(B) * S * 3 * heads * d >= kMaxElems)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *enc_status_string(int status) {
+  switch (status) {
+    case ENC_OK: return "ok";
+    case ENC_ERR_INVALID: return "invalid argument (null pointer or non-positive dimension)";
+    case ENC_ERR_UNSUPPORTED: return "unsupported shape";
+    case ENC_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case ENC_ERR_LAUNCH: return "kernel launch failed";
+    case ENC_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+const char *enc_last_error(void) { return g_last_error.c_str(); }
+
+int enc_abi_version(void) { return 1; }
+
+int enc_saved_layout(const enc_cfg_t *cfg, enc_saved_layout_t *layout) {
+  int r = check_cfg("enc_saved_layout", cfg);
+  if (r) return r;
+  if (!layout) return fail(ENC_ERR_INVALID, "enc_saved_layout: layout is NULL");
+  saved_layout(cfg, layout);
+  return ok();
+}
+
+int enc_layer_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes) {
+  int r = check_cfg("enc_layer_workspace_bytes", cfg);
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "enc_layer_workspace_bytes: bytes is NULL");
+  *bytes = bwd_layout(cfg).total;
+  return ok();
+}
+
+int enc_ln_bwd_workspace_bytes(int rows, int cols, size_t *bytes) {
+  int r = check_dims("enc_ln_bwd_workspace_bytes", {rows, cols});
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "enc_ln_bwd_workspace_bytes: bytes is NULL");
+  *bytes = ln_bwd_ws_bytes(rows, cols);
+  return ok();
+}
+
+int enc_attn_bwd_workspace_bytes(int batch, int seq, int heads, int head_dim, size_t *bytes) {
+  int r = attn_dims("enc_attn_bwd_workspace_bytes", batch, seq, heads, head_dim);
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "enc_attn_bwd_workspace_bytes: bytes is NULL");
+  *bytes = attn_bwd_ws_bytes(batch, seq, heads);
+  return ok();
+}
+
+// ------------------------------------------------------------ forward kernels
+
+int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma, const enc_bf16 *beta, float eps,
+               enc_bf16 *y, float *mean, float *rstd, enc_stream_t stream) {
+  const char *fn = "enc_ln_fwd";
+  int r = check_dims(fn, {rows, cols});
+  if (r) return r;
+  if (cols % 8 || cols > 16384) return fail(ENC_ERR_UNSUPPORTED, "%s: cols must be a multiple of 8 and <= 16384", fn);
+  if (static_cast<long>(rows) * cols >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: too many elements", fn);
+  if (!(eps >= 0.f)) return fail(ENC_ERR_INVALID, "%s: eps must be >= 0", fn);
+  PtrCheck c(fn);
+  c.req(x, "x").req(gamma, "gamma").req(beta, "beta").req(y, "y").req(mean, "mean").req(rstd, "rstd");
+  if (c.code) return c.code;
+  if (!launch_ln_fwd(rows, cols, x, gamma, beta, eps, y, mean, rstd, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+  return launched(fn);
+}
+
+int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv, const enc_bf16 *b_qkv, enc_bf16 *qkv,
+                enc_stream_t stream) {
+  const char *fn = "enc_qkv_fwd";
+  int r = linear_dims(fn, M, {H, A, 3 * A});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(y1, "y1").req(w_qkv, "w_qkv").req(b_qkv, "b_qkv").req(qkv, "qkv");
+  if (c.code) return c.code;
+  if (!gemm_fwd(M, 3 * A, H, y1, w_qkv, b_qkv, nullptr, qkv, nullptr, Epi::kBias, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_attn_fwd(int batch, int seq, int heads, int head_dim, const enc_bf16 *qkv, enc_bf16 *o, float *lse,
+                 enc_stream_t stream) {
+  const char *fn = "enc_attn_fwd";
+  int r = attn_dims(fn, batch, seq, heads, head_dim);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(qkv, "qkv").req(o, "o").req(lse, "lse");
+  if (c.code) return c.code;
+  if (!launch_attn_fwd(batch, seq, heads, head_dim, qkv, o, lse, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported head_dim", fn);
+  return launched(fn);
+}
+
+int enc_oproj_fwd(int M, int A, int H, const enc_bf16 *o, const enc_bf16 *w_o, const enc_bf16 *b_o,
+                  const enc_bf16 *resid, enc_bf16 *h, enc_stream_t stream) {
+  const char *fn = "enc_oproj_fwd";
+  int r = linear_dims(fn, M, {H, A});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(o, "o").req(w_o, "w_o").req(b_o, "b_o").req(resid, "resid").req(h, "h");
+  if (c.code) return c.code;
+  if (!gemm_fwd(M, H, A, o, w_o, b_o, resid, h, nullptr, Epi::kBiasResid, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_mlp_up_fwd(int M, int H, int F, const enc_bf16 *y2, const enc_bf16 *w_1, const enc_bf16 *b_1, enc_bf16 *u,
+                   enc_bf16 *g, enc_stream_t stream) {
+  const char *fn = "enc_mlp_up_fwd";
+  int r = linear_dims(fn, M, {H, F});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(y2, "y2").req(w_1, "w_1").req(b_1, "b_1").req(u, "u").req(g, "g");
+  if (c.code) return c.code;
+  if (!gemm_fwd(M, F, H, y2, w_1, b_1, nullptr, u, g, Epi::kBiasGelu, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2, const enc_bf16 *b_2,
+                     const enc_bf16 *resid, enc_bf16 *out, enc_stream_t stream) {
+  const char *fn = "enc_mlp_down_fwd";
+  int r = linear_dims(fn, M, {H, F});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(g, "g").req(w_2, "w_2").req(b_2, "b_2").req(resid, "resid").req(out, "out");
+  if (c.code) return c.code;
+  if (!gemm_fwd(M, H, F, g, w_2, b_2, resid, out, nullptr, Epi::kBiasResid, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+// ------------------------------------------------------------ backward kernels
+
+int enc_mlp_down_bwd_data(int M, int F, int H, const enc_bf16 *dout, const enc_bf16 *w_2, const enc_bf16 *u,
+                          enc_bf16 *du, enc_stream_t stream) {
+  const char *fn = "enc_mlp_down_bwd_data";
+  int r = linear_dims(fn, M, {H, F});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dout, "dout").req(w_2, "w_2").req(u, "u").req(du, "du");
+  if (c.code) return c.code;
+  if (!gemm_dgrad(M, H, F, dout, w_2, u, du, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du, const enc_bf16 *w_1, enc_bf16 *dy2,
+                        enc_stream_t stream) {
+  const char *fn = "enc_mlp_up_bwd_data";
+  int r = linear_dims(fn, M, {H, F});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(du, "du").req(w_1, "w_1").req(dy2, "dy2");
+  if (c.code) return c.code;
+  if (!gemm_dgrad(M, F, H, du, w_1, nullptr, dy2, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh, const enc_bf16 *w_o, enc_bf16 *do_,
+                       enc_stream_t stream) {
+  const char *fn = "enc_oproj_bwd_data";
+  int r = linear_dims(fn, M, {H, A});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dh, "dh").req(w_o, "w_o").req(do_, "do");
+  if (c.code) return c.code;
+  if (!gemm_dgrad(M, H, A, dh, w_o, nullptr, do_, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *w_qkv, enc_bf16 *dy1,
+                     enc_stream_t stream) {
+  const char *fn = "enc_qkv_bwd_data";
+  int r = linear_dims(fn, M, {H, A, 3 * A});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dqkv, "dqkv").req(w_qkv, "w_qkv").req(dy1, "dy1");
+  if (c.code) return c.code;
+  if (!gemm_dgrad(M, 3 * A, H, dqkv, w_qkv, nullptr, dy1, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_linear_bwd_weight(int M, int N, int K, const enc_bf16 *dY, const enc_bf16 *X, float *dW, float *db,
+                          int accumulate, enc_stream_t stream) {
+  const char *fn = "enc_linear_bwd_weight";
+  int r = linear_dims(fn, M, {N, K});
+  if (r) return r;
+  if (static_cast<long>(N) * K >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: dW exceeds 2^31 elements", fn);
+  PtrCheck c(fn);
+  c.req(dY, "dY").req(X, "X").req(dW, "dW").opt(db, "db");
+  if (c.code) return c.code;
+  if (!gemm_wgrad(M, N, K, dY, X, dW, db, accumulate ? 1 : 0, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_mlp_down_bwd_weight(int M, int F, int H, const enc_bf16 *dout, const enc_bf16 *g, float *dw_2, float *db_2,
+                            int accumulate, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, H, F, dout, g, dw_2, db_2, accumulate, stream);
+}
+
+int enc_mlp_up_bwd_weight(int M, int H, int F, const enc_bf16 *du, const enc_bf16 *y2, float *dw_1, float *db_1,
+                          int accumulate, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, F, H, du, y2, dw_1, db_1, accumulate, stream);
+}
+
+int enc_oproj_bwd_weight(int M, int A, int H, const enc_bf16 *dh, const enc_bf16 *o, float *dw_o, float *db_o,
+                         int accumulate, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, H, A, dh, o, dw_o, db_o, accumulate, stream);
+}
+
+int enc_qkv_bwd_weight(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *y1, float *dw_qkv, float *db_qkv,
+                       int accumulate, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, 3 * A, H, dqkv, y1, dw_qkv, db_qkv, accumulate, stream);
+}
+
+int enc_ln_bwd(int rows, int cols, const enc_bf16 *dy, const enc_bf16 *x, const float *mean, const float *rstd,
+               const enc_bf16 *gamma, const enc_bf16 *dresid, enc_bf16 *dx, float *dgamma, float *dbeta,
+               int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "enc_ln_bwd";
+  int r = check_dims(fn, {rows, cols});
+  if (r) return r;
+  if (cols % 8 || cols > 16384) return fail(ENC_ERR_UNSUPPORTED, "%s: cols must be a multiple of 8 and <= 16384", fn);
+  if (static_cast<long>(rows) * cols >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: too many elements", fn);
+  PtrCheck c(fn);
+  c.req(dy, "dy").req(x, "x").req(mean, "mean").req(rstd, "rstd").req(gamma, "gamma").opt(dresid, "dresid");
+  c.req(dx, "dx").req(dgamma, "dgamma").req(dbeta, "dbeta").req(ws, "ws");
+  if (c.code) return c.code;
+  if (ws_bytes < ln_bwd_ws_bytes(rows, cols))
+    return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, ln_bwd_ws_bytes(rows, cols));
+  if (!launch_ln_bwd(rows, cols, dy, x, mean, rstd, gamma, dresid, dx, dgamma, dbeta, accumulate ? 1 : 0,
+                     static_cast<float *>(ws), as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+  return launched(fn);
+}
+
+int enc_attn_bwd(int batch, int seq, int heads, int head_dim, const enc_bf16 *qkv, const enc_bf16 *o, const float *lse,
+                 const enc_bf16 *do_, enc_bf16 *dqkv, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "enc_attn_bwd";
+  int r = attn_dims(fn, batch, seq, heads, head_dim);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(qkv, "qkv").req(o, "o").req(lse, "lse").req(do_, "do").req(dqkv, "dqkv").req(ws, "ws");
+  if (c.code) return c.code;
+  const size_t need = attn_bwd_ws_bytes(batch, seq, heads);
+  if (ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  if (!launch_attn_bwd(batch, seq, heads, head_dim, qkv, o, lse, do_, dqkv, static_cast<float *>(ws),
+                       as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported head_dim", fn);
+  return launched(fn);
+}
+
+// ------------------------------------------------------------ composites
+
+int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params, const enc_bf16 *x, enc_bf16 *out, void *saved,
+                      void *ws, size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "encoder_layer_fwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if ((r = check_params(fn, params))) return r;
+  PtrCheck c(fn);
+  c.req(x, "x").req(out, "out").req(saved, "saved").opt(ws, "ws");
+  if (c.code) return c.code;
+  (void)ws;
+  (void)ws_bytes;  // the forward chain needs no workspace beyond `saved`
+  enc_saved_layout_t L;
+  saved_layout(cfg, &L);
+  const int M = cfg->batch * cfg->seq, H = cfg->hidden, F = cfg->mlp, A = cfg->heads * cfg->head_dim;
+  const hipStream_t s = as_stream(stream);
+  const enc_params_t &p = *params;
+  bf16_t *y1 = at<bf16_t>(saved, L.y1), *qkv = at<bf16_t>(saved, L.qkv), *o = at<bf16_t>(saved, L.o);
+  bf16_t *h = at<bf16_t>(saved, L.h), *y2 = at<bf16_t>(saved, L.y2), *u = at<bf16_t>(saved, L.u);
+  bf16_t *g = at<bf16_t>(saved, L.g);
+  float *mean1 = at<float>(saved, L.mean1), *rstd1 = at<float>(saved, L.rstd1), *lse = at<float>(saved, L.lse);
+  float *mean2 = at<float>(saved, L.mean2), *rstd2 = at<float>(saved, L.rstd2);
+
+  bool okk = launch_ln_fwd(M, H, x, p.ln1_g, p.ln1_b, cfg->ln_eps, y1, mean1, rstd1, s);
+  okk = okk && gemm_fwd(M, 3 * A, H, y1, p.w_qkv, p.b_qkv, nullptr, qkv, nullptr, Epi::kBias, s);
+  okk = okk && launch_attn_fwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkv, o, lse, s);
+  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, s);
+  okk = okk && launch_ln_fwd(M, H, h, p.ln2_g, p.ln2_b, cfg->ln_eps, y2, mean2, rstd2, s);
+  okk = okk && gemm_fwd(M, F, H, y2, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);
+  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const enc_bf16 *x, const void *saved,
+                      const enc_bf16 *dout, enc_bf16 *dx, const enc_grads_t *grads, int accumulate, void *ws,
+                      size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "encoder_layer_bwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if ((r = check_params(fn, params))) return r;
+  if ((r = check_grads(fn, grads))) return r;
+  PtrCheck c(fn);
+  c.req(x, "x").req(saved, "saved").req(dout, "dout").req(dx, "dx").req(ws, "ws");
+  if (c.code) return c.code;
+  const BwdWs W = bwd_layout(cfg);
+  if (ws_bytes < W.total) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, W.total);
+  enc_saved_layout_t L;
+  saved_layout(cfg, &L);
+  const int M = cfg->batch * cfg->seq, H = cfg->hidden, F = cfg->mlp, A = cfg->heads * cfg->head_dim;
+  const int acc = accumulate ? 1 : 0;
+  const hipStream_t s = as_stream(stream);
+  const enc_params_t &p = *params;
+  const enc_grads_t &gr = *grads;
+  const bf16_t *y1 = at<bf16_t>(saved, L.y1), *qkv = at<bf16_t>(saved, L.qkv), *o = at<bf16_t>(saved, L.o);
+  const bf16_t *h = at<bf16_t>(saved, L.h), *y2 = at<bf16_t>(saved, L.y2), *u = at<bf16_t>(saved, L.u);
+  const bf16_t *g = at<bf16_t>(saved, L.g);
+  const float *mean1 = at<float>(saved, L.mean1), *rstd1 = at<float>(saved, L.rstd1), *lse = at<float>(saved, L.lse);
+  const float *mean2 = at<float>(saved, L.mean2), *rstd2 = at<float>(saved, L.rstd2);
+  bf16_t *du = at<bf16_t>(ws, W.du), *dy2 = at<bf16_t>(ws, W.dy2), *dh = at<bf16_t>(ws, W.dh);
+  bf16_t *dO = at<bf16_t>(ws, W.dO), *dqkv = at<bf16_t>(ws, W.dqkv), *dy1 = at<bf16_t>(ws, W.dy1);
+  float *part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec);
+
+  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                      // du = dout W2 * GELU'(u)
+  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, s);          // dW2, db2
+  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy2, s);               // dy2 = du W1
+  okk = okk && gemm_wgrad(M, F, H, du, y2, gr.w_1, gr.b_1, acc, s);           // dW1, db1
+  okk = okk && launch_ln_bwd(M, H, dy2, h, mean2, rstd2, p.ln2_g, dout, dh, gr.ln2_g, gr.ln2_b, acc, part, s);
+  okk = okk && gemm_dgrad(M, H, A, dh, p.w_o, nullptr, dO, s);                // dO = dh Wo
+  okk = okk && gemm_wgrad(M, H, A, dh, o, gr.w_o, gr.b_o, acc, s);            // dWo, dbo
+  okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkv, o, lse, dO, dqkv, dvec, s);
+  okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, s);       // dy1 = dqkv Wqkv
+  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, s);  // dWqkv, dbqkv
+  okk = okk && launch_ln_bwd(M, H, dy1, x, mean1, rstd1, p.ln1_g, dh, dx, gr.ln1_g, gr.ln1_b, acc, part, s);
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+}  // extern "C"

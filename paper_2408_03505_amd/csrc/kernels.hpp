@@ -1,0 +1,62 @@
+// Host-side launchers of the device kernels (internal to the library).
+// Shapes and pointers are validated by the C-ABI layer before these run;
+// each launcher only configures the grid and enqueues on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace optimus {
+
+typedef uint16_t bf16_t;
+
+// ---- LayerNorm
+bool launch_ln_fwd(int rows, int cols, const bf16_t *x, const bf16_t *gamma, const bf16_t *beta, float eps,
+                   bf16_t *y, float *mean, float *rstd, hipStream_t s);
+int ln_bwd_blocks(int rows);
+size_t ln_bwd_ws_bytes(int rows, int cols);
+bool launch_ln_bwd(int rows, int cols, const bf16_t *dy, const bf16_t *x, const float *mean, const float *rstd,
+                   const bf16_t *gamma, const bf16_t *dresid, bf16_t *dx, float *dgamma, float *dbeta,
+                   int accumulate, float *part, hipStream_t s);
+
+// ---- GEMM family: C[m, n] = sum_k A(m, k) B(n, k)
+enum class Epi : int {
+  kBias = 0,       // Y = acc + bias[n]                       (bf16 out)
+  kBiasResid = 1,  // Y = acc + bias[n] + R[m, n]             (bf16 out)
+  kBiasGelu = 2,   // U = acc + bias[n]; G = GELU(U)          (two bf16 outs)
+  kGeluGrad = 3,   // Y = acc * GELU'(U[m, n])                (bf16 out)
+  kPlain = 4,      // Y = acc                                 (bf16 out)
+  kF32 = 5,        // Wf (+)= acc; optional fused db         (fp32 out)
+};
+
+struct GemmArgs {
+  int M, N, K;
+  const bf16_t *A;  // A(m, k)
+  int lda;
+  const bf16_t *B;  // B(n, k)
+  int ldb;
+  bf16_t *Y;  // bf16 output [M, ldy]
+  int ldy;
+  const bf16_t *bias;  // [N]
+  const bf16_t *R;     // residual / saved pre-activation [M, ldy]
+  bf16_t *Y2;          // second bf16 output (GELU)
+  float *Wf;           // fp32 output [M, ldy]
+  float *db;           // fused row sums of A over k (fp32, [M]) for the weight gradient
+  int accumulate;
+};
+
+// Forward projections: A = X [M, K] row-major, B = W [N, K] row-major.
+bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s);
+// Input gradient: A = dY [M, K] row-major, B(n, k) = W[k, n] (W stored [K, N]).
+bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s);
+// Weight gradient: A(m, k) = dY[k, m], B(n, k) = X[k, n] (contraction over tokens).
+bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s);
+
+// ---- Attention
+bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s);
+size_t attn_bwd_ws_bytes(int B, int S, int heads);
+bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
+                     const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s);
+
+}  // namespace optimus

@@ -82,3 +82,14 @@ CONFIGS = {
     "vit22b_tp8": dict(batch=8, seq=256, hidden=6144, heads=6, head_dim=128, mlp=3072, ln_eps=1e-6),
     "vit22b": dict(batch=8, seq=256, hidden=6144, heads=48, head_dim=128, mlp=24576, ln_eps=1e-6),
 }
+
+
+def random_sparse_sign_bf16(shape, seed, density=0.1):
+    """A seeded tensor with entries in {-1, 0, 1}, each non-zero with
+    probability `density` (sign uniform), stored as bfloat16.  Products of
+    such matrices stay small integers, so fp32 accumulation and bf16 outputs
+    are exact for layout tests."""
+    g = torch.Generator().manual_seed(seed)
+    keep = torch.rand(shape, generator=g) < density
+    sign = torch.randint(0, 2, shape, generator=g, dtype=torch.int32) * 2 - 1
+    return (sign * keep.to(torch.int32)).to(torch.bfloat16)

@@ -1,0 +1,318 @@
+"""Per-kernel parity of the HIP path (through the C ABI) against the oracle.
+
+Every case feeds the same bf16 inputs to the GPU entry point and to the
+float64 oracle.  GEMM layout tests use small-integer inputs so that fp32
+accumulation and bf16 rounding are exact: the GPU result must then equal
+the oracle bit for bit.  Floating-point cases use the parity bar
+max|gpu - ref| / max|ref| <= 2e-2 (activations) or 5e-2 (gradients).
+Output buffers carry guard bands that must stay untouched.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import TOL_ACT, TOL_GRAD, announce, cuda, f64, max_rel
+from paper_2408_03505_amd import binding as B
+from paper_2408_03505_amd.synthetic import random_bf16, random_int_bf16, random_sparse_sign_bf16
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+GUARD = 4096  # elements of guard band after every output
+
+
+def guarded(shape, dtype):
+    """An output tensor followed by a guard band filled with a sentinel."""
+    n = int(np.prod(shape))
+    buf = torch.empty(n + GUARD, dtype=dtype, device="cuda")
+    if dtype == torch.bfloat16:
+        buf.view(torch.int16).fill_(0x7FA5)  # a NaN payload no kernel writes
+    else:
+        buf.view(torch.int32).fill_(0x7FC0DEAD)
+    return buf[:n].view(shape), buf
+
+
+def guard_intact(buf, n):
+    tail = buf[n:]
+    if buf.dtype == torch.bfloat16:
+        return bool((tail.view(torch.int16) == 0x7FA5).all())
+    return bool((tail.view(torch.int32) == 0x7FC0DEAD).all())
+
+
+def exact_equal(got, want):
+    g = f64(got)
+    return bool(np.array_equal(g, want)), float(np.abs(g - want).max())
+
+
+# --------------------------------------------------------------------------- LayerNorm
+
+LN_SHAPES = [(394, 192), (1000, 768), (97, 1280), (2048, 6144), (5, 16384), (3, 8), (1, 64)]
+
+
+@pytest.mark.parametrize("rows,cols", LN_SHAPES)
+def test_ln_fwd(rows, cols):
+    announce(f"ln_fwd rows={rows} cols={cols}")
+    x = random_bf16((rows, cols), 1, 2.0) + 0.5
+    x = x.to(torch.bfloat16)
+    g = (1 + random_bf16((cols,), 2, 0.2).float()).to(torch.bfloat16)
+    b = random_bf16((cols,), 3, 0.2)
+    y, ybuf = guarded((rows, cols), torch.bfloat16)
+    mean, mbuf = guarded((rows,), torch.float32)
+    rstd, rbuf = guarded((rows,), torch.float32)
+    B.enc_ln_fwd(cuda(x), cuda(g), cuda(b), 1e-6, y=y, mean=mean, rstd=rstd)
+    torch.cuda.synchronize()
+    ry, rm, rr = oracle.layernorm_fwd(f64(x), f64(g), f64(b), 1e-6)
+    assert max_rel(f64(y), ry) < TOL_ACT
+    assert np.abs(f64(mean) - rm).max() < 1e-5 * max(1.0, np.abs(rm).max())
+    assert np.abs(f64(rstd) / rr - 1).max() < 1e-5
+    assert guard_intact(ybuf, rows * cols) and guard_intact(mbuf, rows) and guard_intact(rbuf, rows)
+
+
+@pytest.mark.parametrize("rows,cols", [(394, 192), (1000, 768), (300, 6144), (7, 1280), (260, 2048)])
+@pytest.mark.parametrize("with_resid", [True, False])
+def test_ln_bwd(rows, cols, with_resid):
+    announce(f"ln_bwd rows={rows} cols={cols} resid={with_resid}")
+    x = (random_bf16((rows, cols), 11, 1.5).float() - 0.3).to(torch.bfloat16)
+    g = (1 + random_bf16((cols,), 12, 0.2).float()).to(torch.bfloat16)
+    b = random_bf16((cols,), 13, 0.2)
+    dy = random_bf16((rows, cols), 14)
+    dres = random_bf16((rows, cols), 15) if with_resid else None
+    _, mean, rstd = B.enc_ln_fwd(cuda(x), cuda(g), cuda(b), 1e-6)
+    dx, dxbuf = guarded((rows, cols), torch.bfloat16)
+    dg = torch.full((cols,), 0.25, device="cuda")
+    db = torch.full((cols,), -0.5, device="cuda")
+    B.enc_ln_bwd(cuda(dy), cuda(x), mean, rstd, cuda(g), dresid=cuda(dres) if dres is not None else None,
+                 dx=dx, dgamma=dg, dbeta=db, accumulate=True)
+    torch.cuda.synchronize()
+    # the oracle's backward uses its own statistics of the same bf16 x
+    _, rm, rr = oracle.layernorm_fwd(f64(x), f64(g), f64(b), 1e-6)
+    rdx, rdg, rdb = oracle.layernorm_bwd(f64(dy), f64(x), rm, rr, f64(g))
+    if dres is not None:
+        rdx = rdx + f64(dres)
+    assert max_rel(f64(dx), rdx) < TOL_GRAD
+    assert max_rel(f64(dg) - 0.25, rdg) < TOL_GRAD
+    assert max_rel(f64(db) + 0.5, rdb) < TOL_GRAD
+    assert guard_intact(dxbuf, rows * cols)
+
+
+# --------------------------------------------------------------------------- GEMM layouts (exact)
+
+# (M, K_in, N_out) covering one tile, many tiles, ragged rows, K not a
+# multiple of the 64-wide k-step, and the 256x128 tile configuration.
+FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8)]
+
+
+def _sparse(shape, seed, density):
+    return random_sparse_sign_bf16(shape, seed, density)
+
+
+def _density(K):
+    # keep |sum| well inside bf16's exact-integer range (<= 256)
+    return min(0.5, float(np.sqrt(24.0 / K)))
+
+
+@pytest.mark.parametrize("M,K,N", FWD_SHAPES)
+def test_qkv_fwd_exact(M, K, N):
+    announce(f"qkv_fwd exact M={M} K={K} N={N}")
+    N3 = (N // 24) * 24 or 24  # 3A with A a multiple of 8
+    d = _density(K)
+    X, W = _sparse((M, K), 21, d), _sparse((N3, K), 22, d)
+    b = random_int_bf16((N3,), 23, -3, 3)
+    Y, buf = guarded((M, N3), torch.bfloat16)
+    B.enc_qkv_fwd(cuda(X), cuda(W), cuda(b), qkv=Y)
+    torch.cuda.synchronize()
+    ok, err = exact_equal(Y, oracle.linear_fwd(f64(X), f64(W), f64(b)))
+    assert ok, err
+    assert guard_intact(buf, M * N3)
+
+
+@pytest.mark.parametrize("M,K,N", FWD_SHAPES)
+def test_oproj_and_mlp_down_fwd_exact(M, K, N):
+    announce(f"oproj/mlp_down exact M={M} K={K} N={N}")
+    d = _density(K)
+    X, W = _sparse((M, K), 31, d), _sparse((N, K), 32, d)
+    b = random_int_bf16((N,), 33, -3, 3)
+    R = random_int_bf16((M, N), 34, -8, 8)
+    want = oracle.linear_fwd(f64(X), f64(W), f64(b), resid=f64(R))
+    Y, buf = guarded((M, N), torch.bfloat16)
+    B.enc_oproj_fwd(cuda(X), cuda(W), cuda(b), cuda(R), h=Y)
+    torch.cuda.synchronize()
+    ok, err = exact_equal(Y, want)
+    assert ok, err
+    assert guard_intact(buf, M * N)
+    Y2 = B.enc_mlp_down_fwd(cuda(X), cuda(W), cuda(b), cuda(R))
+    torch.cuda.synchronize()
+    ok, err = exact_equal(Y2, want)
+    assert ok, err
+
+
+@pytest.mark.parametrize("M,K,N", FWD_SHAPES[:4])
+def test_mlp_up_fwd(M, K, N):
+    announce(f"mlp_up exact M={M} K={K} N={N}")
+    d = _density(K)
+    X, W = _sparse((M, K), 41, d), _sparse((N, K), 42, d)
+    b = random_int_bf16((N,), 43, -3, 3)
+    u, ubuf = guarded((M, N), torch.bfloat16)
+    g, gbuf = guarded((M, N), torch.bfloat16)
+    B.enc_mlp_up_fwd(cuda(X), cuda(W), cuda(b), u=u, g=g)
+    torch.cuda.synchronize()
+    ru = oracle.linear_fwd(f64(X), f64(W), f64(b))
+    ok, err = exact_equal(u, ru)
+    assert ok, err
+    rg = oracle.gelu(ru)
+    # GELU is applied to the fp32 accumulator, then rounded to bf16
+    assert np.abs(f64(g) - rg).max() <= np.abs(rg).max() * 2 ** -8 + 1e-6
+    assert guard_intact(ubuf, M * N) and guard_intact(gbuf, M * N)
+
+
+# dgrad: dX[M, K] = dY[M, N] W[N, K]
+BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8)]
+
+
+@pytest.mark.parametrize("M,N,K", BWD_DATA_SHAPES)
+def test_bwd_data_exact(M, N, K):
+    announce(f"bwd_data exact M={M} N={N} K={K}")
+    d = _density(N)
+    dY, W = _sparse((M, N), 51, d), _sparse((N, K), 52, d)
+    want = oracle.linear_bwd_data(f64(dY), f64(W))
+    # MLP up: dy2[M, H] = du[M, F] W1[F, H]   (F = N, H = K)
+    out, buf = guarded((M, K), torch.bfloat16)
+    B.enc_mlp_up_bwd_data(cuda(dY), cuda(W), dy2=out)
+    torch.cuda.synchronize()
+    ok, err = exact_equal(out, want)
+    assert ok, err
+    assert guard_intact(buf, M * K)
+    # output projection: dO[M, A] = dh[M, H] Wo[H, A]   (H = N, A = K)
+    ok, err = exact_equal(B.enc_oproj_bwd_data(cuda(dY), cuda(W)), want)
+    assert ok, err
+    # MLP down with GELU'(u) == 1 exactly (u = 8): du = dout W2
+    u = torch.full((M, K), 8.0, dtype=torch.bfloat16)
+    ok, err = exact_equal(B.enc_mlp_down_bwd_data(cuda(dY), cuda(W), cuda(u)), want)
+    assert ok, err
+    if N % 3 == 0 and (N // 3) % 8 == 0:
+        ok, err = exact_equal(B.enc_qkv_bwd_data(cuda(dY), cuda(W)), want)
+        assert ok, err
+
+
+def test_mlp_down_bwd_data_gelu_grad():
+    announce("mlp_down_bwd_data gelu' epilogue")
+    M, H, F = 394, 192, 768
+    dout = random_bf16((M, H), 61)
+    w2 = random_bf16((H, F), 62, 0.05)
+    u = random_bf16((M, F), 63, 1.5)
+    du = B.enc_mlp_down_bwd_data(cuda(dout), cuda(w2), cuda(u))
+    torch.cuda.synchronize()
+    want = oracle.linear_bwd_data(f64(dout), f64(w2)) * oracle.gelu_grad(f64(u))
+    assert max_rel(f64(du), want) < TOL_GRAD
+
+
+# wgrad: dW[N, K] = dY[M, N]^T X[M, K], contraction over M tokens
+WGRAD_SHAPES = [(394, 576, 192), (130, 4096, 4096), (6304, 768, 256), (65, 8, 8), (2048, 1280, 200)]
+
+
+@pytest.mark.parametrize("M,N,K", WGRAD_SHAPES)
+def test_linear_bwd_weight_exact(M, N, K):
+    announce(f"bwd_weight exact M={M} N={N} K={K}")
+    dY = random_int_bf16((M, N), 71, -3, 3)
+    X = random_int_bf16((M, K), 72, -3, 3)
+    rdW, rdb = oracle.linear_bwd_weight(f64(dY), f64(X))
+    dW, wbuf = guarded((N, K), torch.float32)
+    db, bbuf = guarded((N,), torch.float32)
+    B.enc_linear_bwd_weight(cuda(dY), cuda(X), dW=dW, db=db)
+    torch.cuda.synchronize()
+    ok, err = exact_equal(dW, rdW)
+    assert ok, err
+    ok, err = exact_equal(db, rdb)
+    assert ok, err
+    assert guard_intact(wbuf, N * K) and guard_intact(bbuf, N)
+    # accumulate adds onto the existing gradients
+    B.enc_linear_bwd_weight(cuda(dY), cuda(X), dW=dW, db=db, accumulate=True)
+    torch.cuda.synchronize()
+    ok, err = exact_equal(dW, 2 * rdW)
+    assert ok, err
+    ok, err = exact_equal(db, 2 * rdb)
+    assert ok, err
+
+
+def test_named_weight_gradients_match_generic():
+    announce("named bwd_weight aliases")
+    M, H, A, F = 394, 192, 192, 768
+    dout, g = random_int_bf16((M, H), 81, -2, 2), random_int_bf16((M, F), 82, -2, 2)
+    du, y2 = random_int_bf16((M, F), 83, -2, 2), random_int_bf16((M, H), 84, -2, 2)
+    dh, o = random_int_bf16((M, H), 85, -2, 2), random_int_bf16((M, A), 86, -2, 2)
+    dqkv, y1 = random_int_bf16((M, 3 * A), 87, -2, 2), random_int_bf16((M, H), 88, -2, 2)
+    cases = [(B.enc_mlp_down_bwd_weight, dout, g), (B.enc_mlp_up_bwd_weight, du, y2),
+             (B.enc_oproj_bwd_weight, dh, o), (B.enc_qkv_bwd_weight, dqkv, y1)]
+    for fn, dY, X in cases:
+        dW = torch.empty((dY.shape[1], X.shape[1]), device="cuda")
+        db = torch.empty((dY.shape[1],), device="cuda")
+        fn(cuda(dY), cuda(X), dW, db)
+        torch.cuda.synchronize()
+        rdW, rdb = oracle.linear_bwd_weight(f64(dY), f64(X))
+        assert np.array_equal(f64(dW), rdW), fn.__name__
+        assert np.array_equal(f64(db), rdb), fn.__name__
+
+
+def test_linear_bwd_weight_without_db():
+    announce("bwd_weight db=None")
+    dY, X = random_int_bf16((100, 64), 91, -2, 2), random_int_bf16((100, 32), 92, -2, 2)
+    dW, db = B.enc_linear_bwd_weight(cuda(dY), cuda(X), with_db=False)
+    torch.cuda.synchronize()
+    assert db is None
+    assert np.array_equal(f64(dW), oracle.linear_bwd_weight(f64(dY), f64(X))[0])
+
+
+# --------------------------------------------------------------------------- attention
+
+ATTN_CASES = [(2, 197, 3, 64), (1, 257, 2, 80), (2, 256, 2, 128), (1, 1, 1, 64), (3, 7, 2, 80), (1, 65, 1, 128),
+              (1, 129, 2, 64), (2, 300, 1, 80)]
+
+
+def _attn_inputs(Bn, S, nh, d, seed, scale):
+    return random_bf16((Bn * S, 3 * nh * d), seed, scale)
+
+
+@pytest.mark.parametrize("Bn,S,nh,d", ATTN_CASES)
+@pytest.mark.parametrize("scale", [1.0, 3.0])
+def test_attn_fwd(Bn, S, nh, d, scale):
+    announce(f"attn_fwd B={Bn} S={S} heads={nh} d={d} scale={scale}")
+    qkv = _attn_inputs(Bn, S, nh, d, 101, scale)
+    o, obuf = guarded((Bn * S, nh * d), torch.bfloat16)
+    lse, lbuf = guarded((Bn, nh, S), torch.float32)
+    B.enc_attn_fwd(Bn, S, nh, d, cuda(qkv), o=o, lse=lse)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention_fwd(f64(qkv), Bn, S, nh, d)
+    assert max_rel(f64(o), ro) < TOL_ACT
+    assert np.abs(f64(lse) - rl).max() < 2e-3 * max(1.0, np.abs(rl).max())
+    assert guard_intact(obuf, o.numel()) and guard_intact(lbuf, lse.numel())
+
+
+@pytest.mark.parametrize("Bn,S,nh,d", ATTN_CASES)
+def test_attn_bwd(Bn, S, nh, d):
+    announce(f"attn_bwd B={Bn} S={S} heads={nh} d={d}")
+    qkv = _attn_inputs(Bn, S, nh, d, 111, 1.5)
+    dO = random_bf16((Bn * S, nh * d), 112)
+    o, lse = B.enc_attn_fwd(Bn, S, nh, d, cuda(qkv))
+    dqkv, buf = guarded((Bn * S, 3 * nh * d), torch.bfloat16)
+    B.enc_attn_bwd(Bn, S, nh, d, cuda(qkv), o, lse, cuda(dO), dqkv=dqkv)
+    torch.cuda.synchronize()
+    ref = oracle.attention_bwd(f64(qkv), f64(dO), Bn, S, nh, d)
+    got = f64(dqkv)
+    A = nh * d
+    for part, sl in (("dq", slice(0, A)), ("dk", slice(A, 2 * A)), ("dv", slice(2 * A, 3 * A))):
+        assert max_rel(got[:, sl], ref[:, sl]) < TOL_GRAD, part
+    assert guard_intact(buf, dqkv.numel())
+
+
+def test_attn_bwd_is_deterministic():
+    announce("attn_bwd determinism")
+    Bn, S, nh, d = 2, 197, 3, 64
+    qkv = cuda(_attn_inputs(Bn, S, nh, d, 121, 1.0))
+    dO = cuda(random_bf16((Bn * S, nh * d), 122))
+    o, lse = B.enc_attn_fwd(Bn, S, nh, d, qkv)
+    a = B.enc_attn_bwd(Bn, S, nh, d, qkv, o, lse, dO)
+    b = B.enc_attn_bwd(Bn, S, nh, d, qkv, o, lse, dO)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))

@@ -1,0 +1,154 @@
+"""Host-side checks of the C-ABI library: it loads, exports every entry point
+the header declares, sizes buffers consistently, and rejects bad arguments
+with the documented status codes before launching anything.
+
+These tests never launch a kernel.  The argument-error cases pass fake,
+never-dereferenced pointers, so they are skipped whenever a GPU is visible.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2408_03505_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "optimus_enc.h")
+
+no_gpu_only = pytest.mark.skipif(torch.cuda.is_available(), reason="fake-pointer cases run only without a GPU")
+
+VIT22B = dict(batch=8, seq=256, hidden=6144, heads=48, head_dim=128, mlp=24576, ln_eps=1e-6)
+VIT_TINY = dict(batch=2, seq=197, hidden=192, heads=3, head_dim=64, mlp=768, ln_eps=1e-6)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "defined")))
+
+
+def test_header_declares_the_chain():
+    names = declared_functions()
+    for want in ("encoder_layer_fwd", "encoder_layer_bwd", "enc_ln_fwd", "enc_qkv_fwd", "enc_attn_fwd",
+                 "enc_oproj_fwd", "enc_mlp_up_fwd", "enc_mlp_down_fwd", "enc_mlp_down_bwd_data",
+                 "enc_linear_bwd_weight", "enc_mlp_up_bwd_data", "enc_ln_bwd", "enc_oproj_bwd_data",
+                 "enc_attn_bwd", "enc_qkv_bwd_data"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = B.lib()
+    missing = [n for n in declared_functions() if not hasattr(L, n)]
+    assert not missing, missing
+    # the binding covers every declared entry point as well
+    covered = set(B._SIGS) | {"enc_status_string", "enc_last_error"}
+    assert set(declared_functions()) <= covered
+
+
+def test_abi_version_and_status_strings():
+    L = B.lib()
+    assert L.enc_abi_version() == 1
+    for code in (0, -1, -2, -3, -4, -5):
+        assert len(L.enc_status_string(code)) > 0
+    assert L.enc_status_string(7) == b"unknown status"
+
+
+@pytest.mark.parametrize("cfg", [VIT22B, VIT_TINY, dict(VIT22B, heads=6, mlp=3072)])
+def test_saved_layout_is_aligned_and_disjoint(cfg):
+    lay = B.saved_layout(cfg)
+    M = cfg["batch"] * cfg["seq"]
+    H, A, F = cfg["hidden"], cfg["heads"] * cfg["head_dim"], cfg["mlp"]
+    sizes = {"y1": M * H * 2, "mean1": M * 4, "rstd1": M * 4, "qkv": M * 3 * A * 2, "o": M * A * 2,
+             "lse": cfg["batch"] * cfg["heads"] * cfg["seq"] * 4, "h": M * H * 2, "y2": M * H * 2,
+             "mean2": M * 4, "rstd2": M * 4, "u": M * F * 2, "g": M * F * 2}
+    spans = sorted((lay[n], lay[n] + s) for n, s in sizes.items())
+    for n in sizes:
+        assert lay[n] % 256 == 0
+    for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+        assert a1 <= b0
+    assert spans[-1][1] <= lay["total"]
+
+
+def test_workspace_sizes():
+    assert B.layer_workspace_bytes(VIT22B) > 0
+    assert B.ln_bwd_workspace_bytes(2048, 6144) == 256 * 6144 * 8
+    assert B.ln_bwd_workspace_bytes(10, 192) == 10 * 192 * 8
+    assert B.attn_bwd_workspace_bytes(8, 256, 48, 128) == 8 * 48 * 256 * 4
+
+
+def _status(name, *args):
+    L = B.lib()
+    return getattr(L, name)(*args)
+
+
+def test_bad_configs_are_rejected():
+    for bad, code in ((dict(VIT22B, head_dim=96), B.ENC_ERR_UNSUPPORTED),
+                      (dict(VIT22B, hidden=6145), B.ENC_ERR_UNSUPPORTED),
+                      (dict(VIT22B, mlp=100), B.ENC_ERR_UNSUPPORTED),
+                      (dict(VIT22B, batch=0), B.ENC_ERR_INVALID),
+                      (dict(VIT22B, seq=-3), B.ENC_ERR_INVALID),
+                      (dict(VIT22B, hidden=32768), B.ENC_ERR_UNSUPPORTED),
+                      (dict(VIT22B, batch=4096), B.ENC_ERR_UNSUPPORTED)):
+        with pytest.raises(B.EncError) as e:
+            B.layer_workspace_bytes(bad)
+        assert e.value.status == code
+
+
+FAKE = 0x10000  # aligned, never dereferenced
+
+
+@no_gpu_only
+def test_null_and_misaligned_pointers_are_rejected():
+    p, z = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
+    s = ctypes.c_void_p(0)
+    assert _status("enc_ln_fwd", 4, 64, z, p, p, ctypes.c_float(1e-6), p, p, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_ln_fwd", 4, 64, ctypes.c_void_p(FAKE + 2), p, p, ctypes.c_float(1e-6), p, p, p, s) \
+        == B.ENC_ERR_ALIGN
+    assert b"not 16-byte aligned" in B.lib().enc_last_error()
+    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, z, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_attn_fwd", 1, 8, 1, 64, p, z, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, z, z, 0, s) == B.ENC_ERR_INVALID
+    # db may be NULL, but a misaligned db is an error
+    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, p, ctypes.c_void_p(FAKE + 4), 0, s) == B.ENC_ERR_ALIGN
+
+
+@no_gpu_only
+def test_bad_shapes_are_rejected():
+    p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
+    assert _status("enc_ln_fwd", 4, 60, p, p, p, ctypes.c_float(1e-6), p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_ln_fwd", 0, 64, p, p, p, ctypes.c_float(1e-6), p, p, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_ln_fwd", 4, 64, p, p, p, ctypes.c_float(-1.0), p, p, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_attn_fwd", 1, 8, 1, 96, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_qkv_fwd", 8, 60, 64, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_mlp_up_fwd", -1, 64, 64, p, p, p, p, p, s) == B.ENC_ERR_INVALID
+
+
+@no_gpu_only
+def test_small_workspace_is_rejected():
+    p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
+    need = B.ln_bwd_workspace_bytes(16, 64)
+    assert _status("enc_ln_bwd", 16, 64, p, p, p, p, p, ctypes.c_void_p(0), p, p, p, 0, p, need - 1, s) \
+        == B.ENC_ERR_WORKSPACE
+    need = B.attn_bwd_workspace_bytes(1, 8, 1, 64)
+    assert _status("enc_attn_bwd", 1, 8, 1, 64, p, p, p, p, p, p, need - 1, s) == B.ENC_ERR_WORKSPACE
+    cfg = B.make_cfg(VIT_TINY)
+    params = B.EncParams(*[FAKE] * 12)
+    grads = B.EncGrads(*[FAKE] * 12)
+    need = B.layer_workspace_bytes(VIT_TINY)
+    assert _status("encoder_layer_bwd", ctypes.byref(cfg), ctypes.byref(params), p, p, p, p, ctypes.byref(grads),
+                   0, p, need - 1, s) == B.ENC_ERR_WORKSPACE
+    params.w_o = 0
+    assert _status("encoder_layer_fwd", ctypes.byref(cfg), ctypes.byref(params), p, p, p, p, 0, s) \
+        == B.ENC_ERR_INVALID
+    assert b"w_o is NULL" in B.lib().enc_last_error()
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        B.lib()
