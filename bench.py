@@ -38,7 +38,52 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after the timed region, run one device copy of this many MiB "
+                         "(a known-size reference for the HBM byte counters)")
+    ap.add_argument("--summarize", metavar="DIR",
+                    help="print a per-dispatch summary of a rocprofv3 output directory and exit")
     return ap.parse_args()
+
+
+def summarize(d):
+    """Per (kernel, grid) duration and counter summary of a rocprofv3 csv run."""
+    import csv
+    import glob
+    import re
+
+    def rows(pattern):
+        out = []
+        for f in sorted(glob.glob(os.path.join(d, "**", pattern), recursive=True)):
+            with open(f) as fh:
+                out += list(csv.DictReader(fh))
+        return out
+
+    def short(name):
+        name = re.sub(r"\(anonymous namespace\)::", "", name)
+        name = re.sub(r"\(.*\)$", "", name)
+        return name.replace("optimus::", "").replace("void ", "")
+
+    trace = rows("*kernel_trace.csv")
+    groups = {}
+    for r in trace:
+        key = (short(r["Kernel_Name"]), int(r.get("Grid_Size_X", r.get("Grid_Size", 0)) or 0))
+        groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    if groups:
+        print("| kernel | grid | calls | avg us | min us | max us |")
+        print("|---|---|---|---|---|---|")
+        for (k, g), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+            print(f"| {k} | {g} | {len(v)} | {np.mean(v):.2f} | {min(v):.2f} | {max(v):.2f} |")
+    pmc = rows("*counter_collection.csv")
+    if pmc:
+        agg = {}
+        for r in pmc:
+            key = (short(r["Kernel_Name"]), int(r.get("Grid_Size", 0) or 0), r["Counter_Name"])
+            agg.setdefault(key, []).append(float(r["Counter_Value"]))
+        print("\n| kernel | grid | counter | dispatches | avg value |")
+        print("|---|---|---|---|---|")
+        for (k, g, c), v in sorted(agg.items()):
+            print(f"| {k} | {g} | {c} | {len(v)} | {np.mean(v):.1f} |")
 
 
 class Chain:
@@ -152,6 +197,9 @@ def cpu_baseline(cfg, x, params, dout, budget_s):
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args.summarize)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are out of scope "
                                    "(--gpus must be 1)"}), flush=True)
@@ -219,6 +267,12 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "avg_launch_us": round(avg[dom], 2)},
     }
+    if args.copy_mib:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        res["copy_reference_bytes"] = args.copy_mib << 20
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, x, params, dout, args.cpu_budget_s)
     print(json.dumps(res), flush=True)

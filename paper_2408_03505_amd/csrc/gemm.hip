@@ -57,6 +57,64 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int &tm, int &
   tn = in_g / gm;
 }
 
+// Epilogue of one wave tile: lane owns row m and columns nb..nb+3 of each
+// 32x32 fragment (the MFMA is issued as D = Btile * Atile^T).
+template <Epi EPI, int FM, int FN, int WTM, int WTN>
+__device__ __forceinline__ void store_tile(const GemmArgs &p, const f32x16_t (&acc)[FM][FN], int m0, int n0, int wm,
+                                           int wn, int lane) {
+  const int lrow = lane & 31;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int m = m0 + wm * WTM + i * 32 + lrow;
+    if (m >= p.M) continue;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int nb = n0 + wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+        if (nb >= p.N) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][q * 4 + e];
+        const size_t off = static_cast<size_t>(m) * p.ldy + nb;
+        if constexpr (EPI == Epi::kF32) {
+          f32x4_t w{v[0], v[1], v[2], v[3]};
+          if (p.accumulate) w += *reinterpret_cast<const f32x4_t *>(p.Wf + off);
+          *reinterpret_cast<f32x4_t *>(p.Wf + off) = w;
+        } else {
+          if constexpr (EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu) {
+            const u32x2_t bw = *reinterpret_cast<const u32x2_t *>(p.bias + nb);
+            v[0] += lo_bf(bw[0]);
+            v[1] += hi_bf(bw[0]);
+            v[2] += lo_bf(bw[1]);
+            v[3] += hi_bf(bw[1]);
+          }
+          if constexpr (EPI == Epi::kBiasResid) {
+            const u32x2_t rw = *reinterpret_cast<const u32x2_t *>(p.R + off);
+            v[0] += lo_bf(rw[0]);
+            v[1] += hi_bf(rw[0]);
+            v[2] += lo_bf(rw[1]);
+            v[3] += hi_bf(rw[1]);
+          }
+          if constexpr (EPI == Epi::kGeluGrad) {
+            const u32x2_t uw = *reinterpret_cast<const u32x2_t *>(p.R + off);
+            v[0] *= gelu_grad_f(lo_bf(uw[0]));
+            v[1] *= gelu_grad_f(hi_bf(uw[0]));
+            v[2] *= gelu_grad_f(lo_bf(uw[1]));
+            v[3] *= gelu_grad_f(hi_bf(uw[1]));
+          }
+          *reinterpret_cast<u32x2_t *>(p.Y + off) = u32x2_t{pack2(v[0], v[1]), pack2(v[2], v[3])};
+          if constexpr (EPI == Epi::kBiasGelu) {
+            *reinterpret_cast<u32x2_t *>(p.Y2 + off) =
+                u32x2_t{pack2(gelu_f(v[0]), gelu_f(v[1])), pack2(gelu_f(v[2]), gelu_f(v[3]))};
+          }
+        }
+      }
+    }
+  }
+
+}
+
 // Global -> register -> LDS staging of one [ROWS x BK] operand tile.
 template <int ROWS, int BK, int NT, bool TRANS>
 struct TileLoader;
@@ -224,56 +282,7 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_kernel(GemmArgs p) {
     __syncthreads();
   }
 
-  // ---- epilogue: lane owns row m, columns nb..nb+3 of each 32x32 fragment
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * WTM + i * 32 + lrow;
-    if (m >= p.M) continue;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int nb = n0 + wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-        if (nb >= p.N) continue;
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][q * 4 + e];
-        const size_t off = static_cast<size_t>(m) * p.ldy + nb;
-        if constexpr (EPI == Epi::kF32) {
-          f32x4_t w{v[0], v[1], v[2], v[3]};
-          if (p.accumulate) w += *reinterpret_cast<const f32x4_t *>(p.Wf + off);
-          *reinterpret_cast<f32x4_t *>(p.Wf + off) = w;
-        } else {
-          if constexpr (EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu) {
-            const u32x2_t bw = *reinterpret_cast<const u32x2_t *>(p.bias + nb);
-            v[0] += lo_bf(bw[0]);
-            v[1] += hi_bf(bw[0]);
-            v[2] += lo_bf(bw[1]);
-            v[3] += hi_bf(bw[1]);
-          }
-          if constexpr (EPI == Epi::kBiasResid) {
-            const u32x2_t rw = *reinterpret_cast<const u32x2_t *>(p.R + off);
-            v[0] += lo_bf(rw[0]);
-            v[1] += hi_bf(rw[0]);
-            v[2] += lo_bf(rw[1]);
-            v[3] += hi_bf(rw[1]);
-          }
-          if constexpr (EPI == Epi::kGeluGrad) {
-            const u32x2_t uw = *reinterpret_cast<const u32x2_t *>(p.R + off);
-            v[0] *= gelu_grad_f(lo_bf(uw[0]));
-            v[1] *= gelu_grad_f(hi_bf(uw[0]));
-            v[2] *= gelu_grad_f(lo_bf(uw[1]));
-            v[3] *= gelu_grad_f(hi_bf(uw[1]));
-          }
-          *reinterpret_cast<u32x2_t *>(p.Y + off) = u32x2_t{pack2(v[0], v[1]), pack2(v[2], v[3])};
-          if constexpr (EPI == Epi::kBiasGelu) {
-            *reinterpret_cast<u32x2_t *>(p.Y2 + off) =
-                u32x2_t{pack2(gelu_f(v[0]), gelu_f(v[1])), pack2(gelu_f(v[2]), gelu_f(v[3]))};
-          }
-        }
-      }
-    }
-  }
+  store_tile<EPI, FM, FN, WTM, WTN>(p, acc, m0, n0, wm, wn, lane);
 
   // ---- fused bias gradient: row sums of A over all k (column tile 0 only)
   if constexpr (kDb) {
@@ -304,6 +313,264 @@ __global__ __launch_bounds__(WM *WN * 64) void gemm_kernel(GemmArgs p) {
   }
 }
 
+// ===========================================================================
+// Direct-to-LDS pipeline (the large-problem path).
+//
+// Tiles go from HBM straight into LDS with buffer_load_dwordx4 ... lds (no
+// staging registers), STAGES deep, so the loads for k-step t+STAGES-1 are in
+// flight while k-step t runs on the MFMAs.  The buffer resource bounds every
+// operand tensor: rows past its end (tokens past M, weight rows past N, or
+// contraction rows past K of a transposed operand) read as zero.
+//
+// LDS tile layouts (16-byte chunks, XOR-swizzled against bank conflicts):
+//  - contraction-contiguous operand: [row][BK], chunk c of row r stored at
+//    c ^ ((r / RP) % CPR) (RP rows share one 128-byte line); MFMA operands
+//    are single ds_read_b128.
+//  - contraction-strided operand: [BK][ROWS] exactly as in memory, chunk j of
+//    k-row k stored at j ^ 2*(k % 4); MFMA operands are two
+//    ds_read_b64_tr_b16, whose 16-lane transpose delivers lane l the column
+//    (l % 32) of k-rows 8*(l/32) + 0..7.
+// ===========================================================================
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
+
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit dwords, gfx9 data format
+
+template <int BK>
+__device__ __forceinline__ int nt_off(int r, int c) {
+  constexpr int RB = BK * 2;
+  constexpr int RP = (128 / RB) > 0 ? (128 / RB) : 1;
+  constexpr int CPR = BK / 8;
+  return r * RB + ((c ^ ((r / RP) % CPR)) << 4);
+}
+
+template <int ROWS>
+__device__ __forceinline__ int t_off(int k, int j) {
+  return k * (ROWS * 2) + ((j ^ ((k & 3) << 1)) << 4);
+}
+
+// 128-bit buffer resource: base, byte extent and the raw-buffer format word.
+__device__ __forceinline__ u32x4_t make_rsrc(const void *base, uint32_t nbytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return u32x4_t{static_cast<uint32_t>(a), static_cast<uint32_t>(a >> 32) & 0xffffu, nbytes,
+                 static_cast<uint32_t>(kRsrcWord3)};
+}
+
+// One 16-byte-per-lane buffer load written straight to LDS at
+// lds_addr + 16 * lane.  Issued as inline asm so that the compiler does not
+// wrap every later LDS access and barrier in a full vmcnt(0) wait; the
+// kernel waits on vmcnt itself.  M0 (the LDS base of the DMA) is saved and
+// restored around the load; s_nop covers the M0-write hazard.
+__device__ __forceinline__ void buffer_load_lds16(const u32x4_t &rsrc, uint32_t lds_addr, uint32_t voff,
+                                                  uint32_t soff) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+      : "memory");
+}
+
+template <int ROWS, int BK, int NW, bool TRANS>
+struct DirectLoader {
+  static constexpr int BYTES = ROWS * BK * 2;
+  static constexpr int NI = BYTES / (1024 * NW);
+  static_assert(BYTES % (1024 * NW) == 0, "tile bytes must split into whole wave loads");
+  uint32_t voff[NI];
+  u32x4_t rsrc;
+
+  // base/nbytes: the operand tensor; ld its leading dimension (elements);
+  // r0 the first tile row (output row of this operand).
+  __device__ __forceinline__ void init(const bf16_t *base, uint32_t nbytes, int ld, int r0, int wid, int lane) {
+    rsrc = make_rsrc(base, nbytes);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int o = (wid * NI + i) * 1024 + lane * 16;
+      if constexpr (!TRANS) {
+        constexpr int RB = BK * 2, RP = (128 / RB) > 0 ? (128 / RB) : 1, CPR = BK / 8;
+        const int r = o / RB, pch = (o % RB) >> 4;
+        const int c = pch ^ ((r / RP) % CPR);
+        voff[i] = static_cast<uint32_t>(((r0 + r) * static_cast<long>(ld) + c * 8) * 2);
+      } else {
+        const int k = o / (ROWS * 2), pch = (o % (ROWS * 2)) >> 4;
+        const int j = pch ^ ((k & 3) << 1);
+        voff[i] = static_cast<uint32_t>((k * static_cast<long>(ld) + r0 + j * 8) * 2);
+      }
+    }
+  }
+  // Enqueue this wave's share of one stage: soff is the k-step's byte offset.
+  __device__ __forceinline__ void issue(uint32_t tile_addr, uint32_t soff, int wid) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(tile_addr + static_cast<uint32_t>((wid * NI + i) * 1024)),
+                        voff[i], __builtin_amdgcn_readfirstlane(soff));
+  }
+};
+
+__device__ __forceinline__ bf16x8_t lds_read_tr(const lds_char *a, const lds_char *b) {
+  const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      reinterpret_cast<__attribute__((address_space(3))) i16x4_t *>(const_cast<lds_char *>(a)));
+  const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      reinterpret_cast<__attribute__((address_space(3))) i16x4_t *>(const_cast<lds_char *>(b)));
+  typedef short i16x8_t __attribute__((ext_vector_type(8)));
+  const i16x8_t v{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Per-lane LDS byte offsets of one operand's MFMA fragments (stage-relative).
+template <int ROWS, int BK, int F, bool TRANS>
+struct FragAddr {
+  static constexpr int KS = BK / 16;
+  // non-transposed: one address per k-step (fragments add 32 rows);
+  // transposed: two per fragment (k-steps add 16 k-rows).
+  static constexpr int N = TRANS ? 2 * F : KS;
+  int off[N];
+  __device__ __forceinline__ void init(int rbase, int lane) {
+    if constexpr (!TRANS) {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) off[kk] = nt_off<BK>(rbase + (lane & 31), kk * 2 + (lane >> 5));
+    } else {
+      const int k = 8 * (lane >> 5) + ((lane & 15) >> 2);
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const int n = rbase + f * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+        off[2 * f] = t_off<ROWS>(k, n >> 3) + (n & 7) * 2;
+        off[2 * f + 1] = t_off<ROWS>(k + 4, n >> 3) + (n & 7) * 2;
+      }
+    }
+  }
+  __device__ __forceinline__ bf16x8_t get(const lds_char *tile, int f, int kk) const {
+    if constexpr (!TRANS) {
+      return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t *>(tile + off[kk] +
+                                                                                     f * 32 * BK * 2);
+    } else {
+      return lds_read_tr(tile + off[2 * f] + kk * 16 * ROWS * 2, tile + off[2 * f + 1] + kk * 16 * ROWS * 2);
+    }
+  }
+};
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
+__global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, uint32_t a_bytes, uint32_t b_bytes) {
+  constexpr int NW = WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
+  static_assert(STAGES >= 2 && BK % 16 == 0, "pipeline shape");
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
+  lds_char *smem = (lds_char *)(smem_raw);  // generic -> LDS address space
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / WN, wn = wid % WN;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  DirectLoader<BM, BK, NW, AT> la;
+  DirectLoader<BN, BK, NW, BT> lb;
+  la.init(p.A, a_bytes, p.lda, m0, wid, lane);
+  lb.init(p.B, b_bytes, p.ldb, n0, wid, lane);
+  // byte step of one k-step along each operand
+  const uint32_t a_step = AT ? static_cast<uint32_t>(BK) * p.lda * 2 : BK * 2;
+  const uint32_t b_step = BT ? static_cast<uint32_t>(BK) * p.ldb * 2 : BK * 2;
+
+  FragAddr<BM, BK, FM, AT> fa;
+  FragAddr<BN, BK, FN, BT> fb;
+  fa.init(wm * WTM, lane);
+  fb.init(wn * WTN, lane);
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+
+  const int nk = (p.K + BK - 1) / BK;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s) {
+    if (s < nk) {
+      la.issue(lds0 + s * STAGE, s * a_step, wid);
+      lb.issue(lds0 + s * STAGE + A_BYTES, s * b_step, wid);
+    }
+  }
+  constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
+
+  for (int t = 0; t < nk; ++t) {
+    // this wave's loads of k-step t have landed; the barrier makes every
+    // wave's share visible and retires all reads of the buffer refilled next
+    if (t + STAGES - 2 < nk)
+      wait_vmcnt<PER_STAGE * (STAGES - 2)>();
+    else
+      wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    const int tl = t + STAGES - 1;
+    if (tl < nk) {
+      const uint32_t st = lds0 + (tl % STAGES) * STAGE;
+      la.issue(st, tl * a_step, wid);
+      lb.issue(st + A_BYTES, tl * b_step, wid);
+    }
+    const lds_char *As = smem + (t % STAGES) * STAGE;
+    const lds_char *Bs = As + A_BYTES;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8_t af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[i] = fa.get(As, i, kk);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[j] = fb.get(Bs, j, kk);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[j], af[i], acc[i][j]);
+    }
+  }
+  store_tile<EPI, FM, FN, WTM, WTN>(p, acc, m0, n0, wm, wn, lane);
+}
+
+// Deterministic column sums db[n] (+)= sum_m dY[m, n]: block = 64 columns x
+// 4 row groups (every 4th row each), group sums added in a fixed order.
+__global__ __launch_bounds__(256) void colsum_kernel(int M, int N, const bf16_t *__restrict__ dY,
+                                                     float *__restrict__ db, int accumulate) {
+  __shared__ float red[4][64];
+  const int cl = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + cl;
+  float s = 0.f;
+  if (col < N)
+    for (int m = grp; m < M; m += 4) s += bf2f(dY[static_cast<size_t>(m) * N + col]);
+  red[grp][cl] = s;
+  __syncthreads();
+  if (grp == 0 && col < N) {
+    float t = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
+    if (accumulate) t += db[col];
+    db[col] = t;
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
+bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
+  constexpr size_t lds = static_cast<size_t>(STAGES) * (BM + BN) * BK * 2;
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, BK, WM, WN, STAGES, AT, BT, EPI>), dim3(tiles), dim3(WM * WN * 64),
+                     lds, s, a, a_bytes, b_bytes);
+  return true;
+}
+
 template <int BM, int BN, int BK, int WM, int WN, bool AT, bool BT, Epi EPI>
 bool launch_cfg(const GemmArgs &a, hipStream_t s) {
   constexpr int NT = WM * WN * 64;
@@ -323,25 +590,63 @@ bool launch_any(const GemmArgs &a, hipStream_t s) {
   return launch_cfg<128, 128, 64, 2, 2, AT, BT, EPI>(a, s);
 }
 
+// Direct-to-LDS path: pick the tile that minimises (rounds of 256 CUs) x
+// (per-tile cost), where a tile's cost is its MFMA work scaled by a
+// per-shape efficiency (larger wave tiles reuse LDS operands better).
+// Returns false when the operands do not fit the path's constraints.
+template <bool AT, bool BT, Epi EPI>
+bool launch_lds(const GemmArgs &a, hipStream_t s) {
+  constexpr int BK = 32;
+  if ((!AT || !BT) && a.K % BK != 0) return false;  // contiguous-k operands need whole k-steps
+  // operand tensor extents (bytes) bound the buffer loads; keep every offset < 2^32
+  const uint64_t a_rows = AT ? static_cast<uint64_t>(a.K) : static_cast<uint64_t>(a.M);
+  const uint64_t b_rows = BT ? static_cast<uint64_t>(a.K) : static_cast<uint64_t>(a.N);
+  const uint64_t a_bytes = a_rows * a.lda * 2, b_bytes = b_rows * a.ldb * 2;
+  const uint64_t lim = (1ull << 32) - 1;
+  if (a_bytes + 600ull * a.lda * 2 > lim || b_bytes + 600ull * a.ldb * 2 > lim) return false;
+  auto rounds = [](long tiles) { return (tiles + 255) / 256; };
+  const long tL = static_cast<long>((a.M + 255) / 256) * ((a.N + 255) / 256);
+  const long tM = static_cast<long>((a.M + 255) / 256) * ((a.N + 127) / 128);
+  const long tS = static_cast<long>((a.M + 127) / 128) * ((a.N + 127) / 128);
+  const double cL = rounds(tL) * 4.0 / 1.00, cM = rounds(tM) * 2.0 / 0.85, cS = rounds(tS) * 1.0 / 0.65;
+  const uint32_t ab = static_cast<uint32_t>(a_bytes), bb = static_cast<uint32_t>(b_bytes);
+  if (cL <= cM && cL <= cS) return launch_lds_cfg<256, 256, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+  if (cM <= cS) return launch_lds_cfg<256, 128, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+  return launch_lds_cfg<128, 128, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+}
+
 }  // namespace
 
 bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s) {
   switch (epi) {
-    case Epi::kBias: return launch_any<false, false, Epi::kBias>(a, s);
-    case Epi::kBiasResid: return launch_any<false, false, Epi::kBiasResid>(a, s);
-    case Epi::kBiasGelu: return launch_any<false, false, Epi::kBiasGelu>(a, s);
+    case Epi::kBias:
+      return launch_lds<false, false, Epi::kBias>(a, s) || launch_any<false, false, Epi::kBias>(a, s);
+    case Epi::kBiasResid:
+      return launch_lds<false, false, Epi::kBiasResid>(a, s) || launch_any<false, false, Epi::kBiasResid>(a, s);
+    case Epi::kBiasGelu:
+      return launch_lds<false, false, Epi::kBiasGelu>(a, s) || launch_any<false, false, Epi::kBiasGelu>(a, s);
     default: return false;
   }
 }
 
 bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s) {
   switch (epi) {
-    case Epi::kPlain: return launch_any<false, true, Epi::kPlain>(a, s);
-    case Epi::kGeluGrad: return launch_any<false, true, Epi::kGeluGrad>(a, s);
+    case Epi::kPlain:
+      return launch_lds<false, true, Epi::kPlain>(a, s) || launch_any<false, true, Epi::kPlain>(a, s);
+    case Epi::kGeluGrad:
+      return launch_lds<false, true, Epi::kGeluGrad>(a, s) || launch_any<false, true, Epi::kGeluGrad>(a, s);
     default: return false;
   }
 }
 
-bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s) { return launch_any<true, true, Epi::kF32>(a, s); }
+bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s) {
+  if (launch_lds<true, true, Epi::kF32>(a, s)) {
+    // bias gradient: column sums of dY (stored [tokens][a.M]) in a separate pass
+    if (a.db)
+      hipLaunchKernelGGL(colsum_kernel, dim3((a.M + 63) / 64), dim3(256), 0, s, a.K, a.M, a.A, a.db, a.accumulate);
+    return true;
+  }
+  return launch_any<true, true, Epi::kF32>(a, s);
+}
 
 }  // namespace optimus

@@ -101,7 +101,8 @@ def test_ln_bwd(rows, cols, with_resid):
 
 # (M, K_in, N_out) covering one tile, many tiles, ragged rows, K not a
 # multiple of the 64-wide k-step, and the 256x128 tile configuration.
-FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8)]
+FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
+              (2048, 256, 16384), (1000, 96, 4096)]
 
 
 def _sparse(shape, seed, density):
@@ -148,7 +149,7 @@ def test_oproj_and_mlp_down_fwd_exact(M, K, N):
     assert ok, err
 
 
-@pytest.mark.parametrize("M,K,N", FWD_SHAPES[:4])
+@pytest.mark.parametrize("M,K,N", FWD_SHAPES[:4] + FWD_SHAPES[5:])
 def test_mlp_up_fwd(M, K, N):
     announce(f"mlp_up exact M={M} K={K} N={N}")
     d = _density(K)
@@ -168,7 +169,8 @@ def test_mlp_up_fwd(M, K, N):
 
 
 # dgrad: dX[M, K] = dY[M, N] W[N, K]
-BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8)]
+BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8),
+                   (2048, 96, 6144)]
 
 
 @pytest.mark.parametrize("M,N,K", BWD_DATA_SHAPES)
@@ -209,7 +211,8 @@ def test_mlp_down_bwd_data_gelu_grad():
 
 
 # wgrad: dW[N, K] = dY[M, N]^T X[M, K], contraction over M tokens
-WGRAD_SHAPES = [(394, 576, 192), (130, 4096, 4096), (6304, 768, 256), (65, 8, 8), (2048, 1280, 200)]
+WGRAD_SHAPES = [(394, 576, 192), (130, 4096, 4096), (6304, 768, 256), (65, 8, 8), (2048, 1280, 200),
+                (2048, 6144, 1536)]
 
 
 @pytest.mark.parametrize("M,N,K", WGRAD_SHAPES)
