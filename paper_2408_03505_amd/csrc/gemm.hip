@@ -337,18 +337,26 @@ typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit dwords, gfx9 data format
 
+// LDS is 64 banks x 4 bytes (256 bytes per cycle); a 16-lane quarter-wave
+// of ds_read_b128 and a half-wave of ds_read_b64_tr_b16 must hit distinct
+// banks.  nt tiles: RP rows share one 256-byte bank line, so chunk c of row
+// r goes to c ^ ((r / RP) % CPR).  Transposed tiles: k-rows are padded to a
+// power of two (TROWS) and chunk j of k-row k goes to j ^ 4 * (k % 4), which
+// spreads the four k-rows read together over four disjoint 64-byte ranges.
 template <int BK>
-__device__ __forceinline__ int nt_off(int r, int c) {
-  constexpr int RB = BK * 2;
-  constexpr int RP = (128 / RB) > 0 ? (128 / RB) : 1;
-  constexpr int CPR = BK / 8;
-  return r * RB + ((c ^ ((r / RP) % CPR)) << 4);
-}
+struct NtTile {
+  static constexpr int RB = BK * 2;                          // bytes per row
+  static constexpr int RP = (256 / RB) > 0 ? (256 / RB) : 1;  // rows per bank line
+  static constexpr int CPR = BK / 8;                         // 16-byte chunks per row
+  __device__ static __forceinline__ int off(int r, int c) { return r * RB + ((c ^ ((r / RP) % CPR)) << 4); }
+};
 
 template <int ROWS>
-__device__ __forceinline__ int t_off(int k, int j) {
-  return k * (ROWS * 2) + ((j ^ ((k & 3) << 1)) << 4);
-}
+struct TTile {
+  static constexpr int TROWS = ROWS <= 128 ? 128 : 256;  // padded k-row length
+  static_assert(ROWS <= 256 && ROWS % 32 == 0, "transposed tile width");
+  __device__ static __forceinline__ int off(int k, int j) { return k * (TROWS * 2) + ((j ^ ((k & 3) << 2)) << 4); }
+};
 
 // 128-bit buffer resource: base, byte extent and the raw-buffer format word.
 __device__ __forceinline__ u32x4_t make_rsrc(const void *base, uint32_t nbytes) {
@@ -378,37 +386,45 @@ __device__ __forceinline__ void buffer_load_lds16(const u32x4_t &rsrc, uint32_t 
 
 template <int ROWS, int BK, int NW, bool TRANS>
 struct DirectLoader {
-  static constexpr int BYTES = ROWS * BK * 2;
+  // LDS bytes of one stage of this operand (transposed tiles are padded)
+  static constexpr int BYTES = TRANS ? TTile<ROWS>::TROWS * BK * 2 : ROWS * BK * 2;
   static constexpr int NI = BYTES / (1024 * NW);
   static_assert(BYTES % (1024 * NW) == 0, "tile bytes must split into whole wave loads");
   uint32_t voff[NI];
+  uint32_t live;  // bit i: this lane's chunk of load i is real data (not padding)
   u32x4_t rsrc;
 
   // base/nbytes: the operand tensor; ld its leading dimension (elements);
   // r0 the first tile row (output row of this operand).
   __device__ __forceinline__ void init(const bf16_t *base, uint32_t nbytes, int ld, int r0, int wid, int lane) {
     rsrc = make_rsrc(base, nbytes);
+    live = 0;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int o = (wid * NI + i) * 1024 + lane * 16;
       if constexpr (!TRANS) {
-        constexpr int RB = BK * 2, RP = (128 / RB) > 0 ? (128 / RB) : 1, CPR = BK / 8;
-        const int r = o / RB, pch = (o % RB) >> 4;
-        const int c = pch ^ ((r / RP) % CPR);
+        using T = NtTile<BK>;
+        const int r = o / T::RB, pch = (o % T::RB) >> 4;
+        const int c = pch ^ ((r / T::RP) % T::CPR);
         voff[i] = static_cast<uint32_t>(((r0 + r) * static_cast<long>(ld) + c * 8) * 2);
+        live |= 1u << i;
       } else {
-        const int k = o / (ROWS * 2), pch = (o % (ROWS * 2)) >> 4;
-        const int j = pch ^ ((k & 3) << 1);
+        constexpr int TR = TTile<ROWS>::TROWS;
+        const int k = o / (TR * 2), pch = (o % (TR * 2)) >> 4;
+        const int j = pch ^ ((k & 3) << 2);
         voff[i] = static_cast<uint32_t>((k * static_cast<long>(ld) + r0 + j * 8) * 2);
+        if (j * 8 < ROWS) live |= 1u << i;
       }
     }
   }
   // Enqueue this wave's share of one stage: soff is the k-step's byte offset.
   __device__ __forceinline__ void issue(uint32_t tile_addr, uint32_t soff, int wid) {
 #pragma unroll
-    for (int i = 0; i < NI; ++i)
-      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(tile_addr + static_cast<uint32_t>((wid * NI + i) * 1024)),
-                        voff[i], __builtin_amdgcn_readfirstlane(soff));
+    for (int i = 0; i < NI; ++i) {
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(tile_addr + static_cast<uint32_t>((wid * NI + i) * 1024));
+      const uint32_t so = __builtin_amdgcn_readfirstlane(soff);
+      if (!TRANS || TTile<ROWS>::TROWS == ROWS || ((live >> i) & 1u)) buffer_load_lds16(rsrc, dst, voff[i], so);
+    }
   }
 };
 
@@ -422,11 +438,11 @@ __device__ __forceinline__ bf16x8_t lds_read_tr(const lds_char *a, const lds_cha
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
-template <int N>
+// s_waitcnt vmcnt(N) lgkmcnt(L) (gfx9 encoding; L = 15 leaves LDS alone).
+template <int N, int L = 15>
 __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  static_assert(N >= 0 && N < 64 && L >= 0 && L < 16, "waitcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (L << 8));
 }
 
 // Per-lane LDS byte offsets of one operand's MFMA fragments (stage-relative).
@@ -440,14 +456,14 @@ struct FragAddr {
   __device__ __forceinline__ void init(int rbase, int lane) {
     if constexpr (!TRANS) {
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) off[kk] = nt_off<BK>(rbase + (lane & 31), kk * 2 + (lane >> 5));
+      for (int kk = 0; kk < KS; ++kk) off[kk] = NtTile<BK>::off(rbase + (lane & 31), kk * 2 + (lane >> 5));
     } else {
       const int k = 8 * (lane >> 5) + ((lane & 15) >> 2);
 #pragma unroll
       for (int f = 0; f < F; ++f) {
         const int n = rbase + f * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-        off[2 * f] = t_off<ROWS>(k, n >> 3) + (n & 7) * 2;
-        off[2 * f + 1] = t_off<ROWS>(k + 4, n >> 3) + (n & 7) * 2;
+        off[2 * f] = TTile<ROWS>::off(k, n >> 3) + (n & 7) * 2;
+        off[2 * f + 1] = TTile<ROWS>::off(k + 4, n >> 3) + (n & 7) * 2;
       }
     }
   }
@@ -456,22 +472,43 @@ struct FragAddr {
       return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t *>(tile + off[kk] +
                                                                                      f * 32 * BK * 2);
     } else {
-      return lds_read_tr(tile + off[2 * f] + kk * 16 * ROWS * 2, tile + off[2 * f + 1] + kk * 16 * ROWS * 2);
+      constexpr int TR = TTile<ROWS>::TROWS;
+      return lds_read_tr(tile + off[2 * f] + kk * 16 * TR * 2, tile + off[2 * f + 1] + kk * 16 * TR * 2);
     }
   }
 };
+
+// Scheduling hint for one k-step: spread the NR LDS reads of the next
+// k-step's fragments evenly between the NM MFMAs of this k-step, so that the
+// reads have a whole k-step of MFMA work to land in.
+template <int NM, int NR, int M = 0>
+__device__ __forceinline__ void interleave_reads() {
+#ifndef OPTIMUS_NO_SCHED_GROUPS
+  if constexpr (M < NM) {
+    constexpr int per = (NR + NM - 1) / NM;
+    constexpr int done = M * per < NR ? M * per : NR;
+    constexpr int r = (NR - done) < per ? (NR - done) : per;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // then r LDS reads
+    interleave_reads<NM, NR, M + 1>();
+  }
+#endif
+}
 
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
 __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, uint32_t a_bytes, uint32_t b_bytes) {
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
+  constexpr int KS = BK / 16;
+  constexpr int A_BYTES = DirectLoader<BM, BK, NW, AT>::BYTES, B_BYTES = DirectLoader<BN, BK, NW, BT>::BYTES;
+  constexpr int STAGE = A_BYTES + B_BYTES;
   static_assert(STAGES >= 2 && BK % 16 == 0, "pipeline shape");
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
-  lds_char *smem = (lds_char *)(smem_raw);  // generic -> LDS address space
+  const lds_char *smem = (const lds_char *)(smem_raw);  // generic -> LDS address space
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int wm = wid / WN, wn = wid % WN;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tm, tn;
@@ -499,6 +536,7 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
 
   const int nk = (p.K + BK - 1) / BK;
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+  constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s) {
     if (s < nk) {
@@ -506,18 +544,28 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       lb.issue(lds0 + s * STAGE + A_BYTES, s * b_step, wid);
     }
   }
-  constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
+  // k-step 0 resident for every wave
+  if (STAGES - 1 < nk)
+    wait_vmcnt<PER_STAGE * (STAGES - 2)>();
+  else
+    wait_vmcnt<0>();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+
+  // Fragments are double-buffered in registers: the next k-step's LDS reads
+  // are issued behind the current k-step's MFMAs.  The stage barrier sits
+  // after the last k-step's MFMAs are issued, so their execution covers the
+  // barrier and the first reads of the next stage.
+  bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) af[0][i] = fa.get(smem, i, 0);
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bfr[0][j] = fb.get(smem + A_BYTES, j, 0);
 
   for (int t = 0; t < nk; ++t) {
-    // this wave's loads of k-step t have landed; the barrier makes every
-    // wave's share visible and retires all reads of the buffer refilled next
-    if (t + STAGES - 2 < nk)
-      wait_vmcnt<PER_STAGE * (STAGES - 2)>();
-    else
-      wait_vmcnt<0>();
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+    // refill the buffer of k-step t-1 (every wave finished reading it
+    // before the barrier that ended k-step t-1)
     const int tl = t + STAGES - 1;
     if (tl < nk) {
       const uint32_t st = lds0 + (tl % STAGES) * STAGE;
@@ -525,45 +573,103 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       lb.issue(st + A_BYTES, tl * b_step, wid);
     }
     const lds_char *As = smem + (t % STAGES) * STAGE;
-    const lds_char *Bs = As + A_BYTES;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8_t af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) af[i] = fa.get(As, i, kk);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[j] = fb.get(Bs, j, kk);
+    for (int kk = 0; kk < KS; ++kk) {
+      const int c = kk & 1, n = c ^ 1;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[j], af[i], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[c][j], af[c][i], acc[i][j]);
+      if (kk + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[n][i] = fa.get(As, i, kk + 1);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[n][j] = fb.get(As + A_BYTES, j, kk + 1);
+        interleave_reads<FM * FN, (FM + FN) * (AT || BT ? 2 : 1)>();
+      } else if (t + 1 < nk) {
+        // also retire this wave's LDS reads of k-step t before the barrier
+        if (t + STAGES - 1 < nk)
+          wait_vmcnt<PER_STAGE * (STAGES - 2), 0>();
+        else
+          wait_vmcnt<0, 0>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const lds_char *Ns = smem + ((t + 1) % STAGES) * STAGE;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[n][i] = fa.get(Ns, i, 0);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[n][j] = fb.get(Ns + A_BYTES, j, 0);
+      }
+    }
+    if constexpr (KS % 2 == 1) {
+      // odd k-steps per stage: the next stage's fragments sit in buffer 1
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[0][i] = af[1][i];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[0][j] = bfr[1][j];
     }
   }
   store_tile<EPI, FM, FN, WTM, WTN>(p, acc, m0, n0, wm, wn, lane);
 }
 
-// Deterministic column sums db[n] (+)= sum_m dY[m, n]: block = 64 columns x
-// 4 row groups (every 4th row each), group sums added in a fixed order.
+// Deterministic column sums db[n] (+)= sum_m dY[m, n].  A block owns 64
+// columns; its 256 threads are 8 column chunks (16-byte loads of 8 columns)
+// x 32 row groups (rows g, g + 32, ...).  The 32 partial sums of each column
+// are then added in a fixed order through LDS.
+constexpr int kColsumCols = 64, kColsumGroups = 32;
+
 __global__ __launch_bounds__(256) void colsum_kernel(int M, int N, const bf16_t *__restrict__ dY,
                                                      float *__restrict__ db, int accumulate) {
-  __shared__ float red[4][64];
-  const int cl = threadIdx.x & 63, grp = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + cl;
-  float s = 0.f;
-  if (col < N)
-    for (int m = grp; m < M; m += 4) s += bf2f(dY[static_cast<size_t>(m) * N + col]);
-  red[grp][cl] = s;
+  __shared__ float red[kColsumGroups][kColsumCols + 1];
+  const int chunk = threadIdx.x & 7, grp = threadIdx.x >> 3;
+  const int c0 = blockIdx.x * kColsumCols + chunk * 8;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (c0 < N) {
+    const bf16_t *col = dY + c0;
+    int m = grp;
+#pragma unroll 1
+    for (; m + 3 * kColsumGroups < M; m += 4 * kColsumGroups) {
+      u32x4_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = ldg16(col + static_cast<size_t>(m + u * kColsumGroups) * N);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s[2 * e] += lo_bf(v[u][e]);
+          s[2 * e + 1] += hi_bf(v[u][e]);
+        }
+    }
+    for (; m < M; m += kColsumGroups) {
+      const u32x4_t v = ldg16(col + static_cast<size_t>(m) * N);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[2 * e] += lo_bf(v[e]);
+        s[2 * e + 1] += hi_bf(v[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[grp][chunk * 8 + e] = s[e];
   __syncthreads();
-  if (grp == 0 && col < N) {
-    float t = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
-    if (accumulate) t += db[col];
-    db[col] = t;
+  if (threadIdx.x < kColsumCols) {
+    const int col = blockIdx.x * kColsumCols + threadIdx.x;
+    float t = 0.f;
+#pragma unroll 8
+    for (int g = 0; g < kColsumGroups; ++g) t += red[g][threadIdx.x];
+    if (col < N) {
+      if (accumulate) t += db[col];
+      db[col] = t;
+    }
   }
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
 bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
-  constexpr size_t lds = static_cast<size_t>(STAGES) * (BM + BN) * BK * 2;
+  constexpr int NW = WM * WN;
+  constexpr size_t lds = static_cast<size_t>(STAGES) *
+                         (DirectLoader<BM, BK, NW, AT>::BYTES + DirectLoader<BN, BK, NW, BT>::BYTES);
   static_assert(lds <= 160 * 1024, "LDS budget");
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, BK, WM, WN, STAGES, AT, BT, EPI>), dim3(tiles), dim3(WM * WN * 64),
@@ -591,12 +697,14 @@ bool launch_any(const GemmArgs &a, hipStream_t s) {
 }
 
 // Direct-to-LDS path: pick the tile that minimises (rounds of 256 CUs) x
-// (per-tile cost), where a tile's cost is its MFMA work scaled by a
-// per-shape efficiency (larger wave tiles reuse LDS operands better).
+// (tile area / per-tile efficiency).  Measured on MI355X at the ViT-22B layer
+// shapes: 8-wave 256x256 tiles are the most efficient per tile, 8-wave
+// 256x192 tiles divide the 6144-wide and 18432-wide outputs into whole
+// rounds, and 4-wave 128x128 tiles serve small problems.
 // Returns false when the operands do not fit the path's constraints.
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s) {
-  constexpr int BK = 32;
+  constexpr int BK = 64;
   if ((!AT || !BT) && a.K % BK != 0) return false;  // contiguous-k operands need whole k-steps
   // operand tensor extents (bytes) bound the buffer loads; keep every offset < 2^32
   const uint64_t a_rows = AT ? static_cast<uint64_t>(a.K) : static_cast<uint64_t>(a.M);
@@ -604,15 +712,15 @@ bool launch_lds(const GemmArgs &a, hipStream_t s) {
   const uint64_t a_bytes = a_rows * a.lda * 2, b_bytes = b_rows * a.ldb * 2;
   const uint64_t lim = (1ull << 32) - 1;
   if (a_bytes + 600ull * a.lda * 2 > lim || b_bytes + 600ull * a.ldb * 2 > lim) return false;
-  auto rounds = [](long tiles) { return (tiles + 255) / 256; };
-  const long tL = static_cast<long>((a.M + 255) / 256) * ((a.N + 255) / 256);
-  const long tM = static_cast<long>((a.M + 255) / 256) * ((a.N + 127) / 128);
-  const long tS = static_cast<long>((a.M + 127) / 128) * ((a.N + 127) / 128);
-  const double cL = rounds(tL) * 4.0 / 1.00, cM = rounds(tM) * 2.0 / 0.85, cS = rounds(tS) * 1.0 / 0.65;
+  auto cost = [&](int bm, int bn, double eff) {
+    const long tiles = static_cast<long>((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+    return static_cast<double>((tiles + 255) / 256) * bm * bn / eff;
+  };
+  const double cL = cost(256, 256, 1.0), cM = cost(256, 192, 0.95), cS = cost(128, 128, 0.75);
   const uint32_t ab = static_cast<uint32_t>(a_bytes), bb = static_cast<uint32_t>(b_bytes);
-  if (cL <= cM && cL <= cS) return launch_lds_cfg<256, 256, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
-  if (cM <= cS) return launch_lds_cfg<256, 128, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
-  return launch_lds_cfg<128, 128, BK, 2, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+  if (cL <= cM && cL <= cS) return launch_lds_cfg<256, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);
+  if (cM <= cS) return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
+  return launch_lds_cfg<128, 128, BK, 2, 2, 2, AT, BT, EPI>(a, ab, bb, s);
 }
 
 }  // namespace
@@ -643,7 +751,8 @@ bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s) {
   if (launch_lds<true, true, Epi::kF32>(a, s)) {
     // bias gradient: column sums of dY (stored [tokens][a.M]) in a separate pass
     if (a.db)
-      hipLaunchKernelGGL(colsum_kernel, dim3((a.M + 63) / 64), dim3(256), 0, s, a.K, a.M, a.A, a.db, a.accumulate);
+      hipLaunchKernelGGL(colsum_kernel, dim3((a.M + kColsumCols - 1) / kColsumCols), dim3(256), 0, s, a.K, a.M, a.A,
+                         a.db, a.accumulate);
     return true;
   }
   return launch_any<true, true, Epi::kF32>(a, s);

@@ -100,9 +100,10 @@ def test_ln_bwd(rows, cols, with_resid):
 # --------------------------------------------------------------------------- GEMM layouts (exact)
 
 # (M, K_in, N_out) covering one tile, many tiles, ragged rows, K not a
-# multiple of the 64-wide k-step, and the 256x128 tile configuration.
+# multiple of the 64-wide k-step (register-staged path) and each tile
+# configuration of the direct-to-LDS path (256x256, 256x192, 128x128).
 FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
-              (2048, 256, 16384), (1000, 96, 4096)]
+              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144)]
 
 
 def _sparse(shape, seed, density):
@@ -170,7 +171,7 @@ def test_mlp_up_fwd(M, K, N):
 
 # dgrad: dX[M, K] = dY[M, N] W[N, K]
 BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8),
-                   (2048, 96, 6144)]
+                   (2048, 96, 6144), (2048, 128, 6144)]
 
 
 @pytest.mark.parametrize("M,N,K", BWD_DATA_SHAPES)
