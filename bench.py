@@ -43,11 +43,91 @@ def parse():
                          "(a known-size reference for the HBM byte counters)")
     ap.add_argument("--summarize", metavar="DIR",
                     help="print a per-dispatch summary of a rocprofv3 output directory and exit")
+    ap.add_argument("--pmc-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
+                         "--copy-mib into per-kernel HBM bytes and print them as markdown")
     return ap.parse_args()
 
 
-def summarize(d):
-    """Per (kernel, grid) duration and counter summary of a rocprofv3 csv run."""
+# GPU dispatches of each chain entry, in launch order
+DISPATCHES = {"ln1_fwd": 1, "qkv_fwd": 1, "attn_fwd": 1, "oproj_fwd": 1, "ln2_fwd": 1, "mlp_up_fwd": 1,
+              "mlp_down_fwd": 1, "mlp_down_bwd_data": 1, "mlp_down_bwd_weight": 1, "mlp_up_bwd_data": 1,
+              "mlp_up_bwd_weight": 1, "ln2_bwd": 2, "oproj_bwd_data": 1, "oproj_bwd_weight": 1, "attn_bwd": 2,
+              "qkv_bwd_data": 1, "qkv_bwd_weight": 1, "ln1_bwd": 2}
+LIB_KERNELS = ("gemm_kernel", "gemm_lds_kernel", "attn_fwd_kernel", "attn_bwd_dq_kernel", "attn_bwd_dkdv_kernel",
+               "ln_fwd_kernel", "ln_bwd_kernel", "ln_bwd_reduce_kernel")
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "vit22b_layer_hbm_traffic.md")
+
+
+def source_hash():
+    """sha256 over the HIP sources: traffic counters describe these kernels only."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2408_03505_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    rows = []
+    for f in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def pmc_traffic(fetch_dir, write_dir, copy_bytes):
+    """Per-entry HBM bytes per launch from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch), each scaled by what the counter reports for a device copy of
+    copy_bytes in the same run."""
+    vals = {}
+    for d, ctr in ((fetch_dir, "FETCH_SIZE"), (write_dir, "WRITE_SIZE")):
+        rows = [r for r in _counter_rows(d) if r["Counter_Name"] == ctr]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        scale = copy_bytes / (max(copies) * 1024.0)
+        lib = sorted(((int(r["Dispatch_Id"]), float(r["Counter_Value"])) for r in rows
+                      if any(k in r["Kernel_Name"] for k in LIB_KERNELS)), key=lambda t: t[0])
+        per_step = sum(DISPATCHES.values())
+        if len(lib) % per_step:
+            raise RuntimeError(f"{len(lib)} library dispatches is not a whole number of steps")
+        steps = len(lib) // per_step
+        out = {n: 0.0 for n in DISPATCHES}
+        for st in range(steps):
+            i = st * per_step
+            for n, k in DISPATCHES.items():
+                out[n] += sum(v for _, v in lib[i:i + k]) * 1024.0 * scale / steps
+                i += k
+        vals[ctr] = (out, scale)
+    return vals
+
+
+def read_traffic(entry):
+    """HBM bytes per launch of one entry from the committed profile, or None
+    when the profile is missing or was taken on different kernel sources."""
+    if not os.path.exists(TRAFFIC_MD):
+        return None
+    text = open(TRAFFIC_MD).read()
+    if f"source-sha256: {source_hash()}" not in text:
+        return None
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 4 and cells[0] == entry:
+            try:
+                return float(cells[3])
+            except ValueError:
+                return None
+    return None
+
+
+def summarize(d, skip_steps=0):
+    """Per (kernel, grid) duration and counter summary of a rocprofv3 csv run;
+    for a kernel trace of this bench also the average duration of each chain
+    entry (dispatches mapped by launch order, the first skip_steps steps,
+    i.e. the warm-up, left out)."""
     import csv
     import glob
     import re
@@ -65,6 +145,23 @@ def summarize(d):
         return name.replace("optimus::", "").replace("void ", "")
 
     trace = rows("*kernel_trace.csv")
+    lib = sorted(((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+                  for r in trace if any(k in r["Kernel_Name"] for k in LIB_KERNELS)))
+    per_step = sum(DISPATCHES.values())
+    if lib and len(lib) % per_step == 0:
+        steps = len(lib) // per_step
+        acc = {n: [] for n in DISPATCHES}
+        for st in range(skip_steps, steps):
+            i = st * per_step
+            for n, k in DISPATCHES.items():
+                acc[n].append(sum(v for _, v in lib[i:i + k]))
+                i += k
+        print(f"per chain entry, steps {skip_steps}..{steps - 1} (device time of its dispatches):\n")
+        print("| entry | dispatches | avg us | min us | max us |")
+        print("|---|---|---|---|---|")
+        for n, v in acc.items():
+            print(f"| {n} | {DISPATCHES[n]} | {np.mean(v):.2f} | {min(v):.2f} | {max(v):.2f} |")
+        print()
     groups = {}
     for r in trace:
         key = (short(r["Kernel_Name"]), int(r.get("Grid_Size_X", r.get("Grid_Size", 0)) or 0))
@@ -198,7 +295,20 @@ def cpu_baseline(cfg, x, params, dout, budget_s):
 def main():
     args = parse()
     if args.summarize:
-        summarize(args.summarize)
+        summarize(args.summarize, skip_steps=args.warmup)
+        return
+    if args.pmc_traffic:
+        from paper_2408_03505_amd.synthetic import CONFIGS
+        vals = pmc_traffic(args.pmc_traffic[0], args.pmc_traffic[1], args.copy_mib << 20)
+        work = kernel_work(CONFIGS[args.config])
+        (fetch, fs), (write, ws) = vals["FETCH_SIZE"], vals["WRITE_SIZE"]
+        print(f"source-sha256: {source_hash()}")
+        print(f"copy-reference-bytes: {args.copy_mib << 20}  fetch-scale: {fs:.4f}  write-scale: {ws:.4f}\n")
+        print("| entry | FETCH bytes | WRITE bytes | traffic bytes | algorithmic bytes | traffic / algorithmic |")
+        print("|---|---|---|---|---|---|")
+        for n in DISPATCHES:
+            t = fetch[n] + write[n]
+            print(f"| {n} | {fetch[n]:.0f} | {write[n]:.0f} | {t:.0f} | {work[n][1]} | {t / work[n][1]:.2f} |")
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are out of scope "
@@ -243,7 +353,8 @@ def main():
     ms = wall / K * 1e3
     tflops = flops_step / (wall / K) / 1e12
 
-    dom = max(names, key=lambda n: avg[n])
+    # the dominant kernel: the single-dispatch entry with the largest average time
+    dom = max((n for n in names if DISPATCHES[n] == 1), key=lambda n: avg[n])
     dflops = work[dom][0]
     achieved = dflops / (avg[dom] * 1e-6) / 1e12
     per_kernel = {n: {"p50_us": round(p50[n], 2),
@@ -264,7 +375,8 @@ def main():
         "max_kernel_p50_us": round(max(p50.values()), 2),
         "per_kernel": per_kernel,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": read_traffic(dom) if args.config == "vit22b" else None,
                      "avg_launch_us": round(avg[dom], 2)},
     }
     if args.copy_mib:

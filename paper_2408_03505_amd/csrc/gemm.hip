@@ -534,6 +534,15 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
+  // Weight gradient: the bias gradient db[m] = sum_k A(m, k) is summed from
+  // the A fragments already in registers by the first wave column of the
+  // first column tile (fixed order: deterministic).
+  constexpr bool kDb = (EPI == Epi::kF32);
+  const bool do_db = kDb && p.db != nullptr && tn == 0 && wn == 0;
+  float dbacc[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) dbacc[i] = 0.f;
+
   const int nk = (p.K + BK - 1) / BK;
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
@@ -580,6 +589,16 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[c][j], af[c][i], acc[i][j]);
+      if constexpr (kDb) {
+        if (do_db) {
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const u32x4_t w = __builtin_bit_cast(u32x4_t, af[c][i]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dbacc[i] += lo_bf(w[e]) + hi_bf(w[e]);
+          }
+        }
+      }
       if (kk + 1 < KS) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) af[n][i] = fa.get(As, i, kk + 1);
@@ -611,56 +630,15 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
     }
   }
   store_tile<EPI, FM, FN, WTM, WTN>(p, acc, m0, n0, wm, wn, lane);
-}
-
-// Deterministic column sums db[n] (+)= sum_m dY[m, n].  A block owns 64
-// columns; its 256 threads are 8 column chunks (16-byte loads of 8 columns)
-// x 32 row groups (rows g, g + 32, ...).  The 32 partial sums of each column
-// are then added in a fixed order through LDS.
-constexpr int kColsumCols = 64, kColsumGroups = 32;
-
-__global__ __launch_bounds__(256) void colsum_kernel(int M, int N, const bf16_t *__restrict__ dY,
-                                                     float *__restrict__ db, int accumulate) {
-  __shared__ float red[kColsumGroups][kColsumCols + 1];
-  const int chunk = threadIdx.x & 7, grp = threadIdx.x >> 3;
-  const int c0 = blockIdx.x * kColsumCols + chunk * 8;
-  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (c0 < N) {
-    const bf16_t *col = dY + c0;
-    int m = grp;
-#pragma unroll 1
-    for (; m + 3 * kColsumGroups < M; m += 4 * kColsumGroups) {
-      u32x4_t v[4];
+  if constexpr (kDb) {
+    if (do_db) {
+      // lane l and l ^ 32 hold the two token halves of row (l % 32)
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = ldg16(col + static_cast<size_t>(m + u * kColsumGroups) * N);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s[2 * e] += lo_bf(v[u][e]);
-          s[2 * e + 1] += hi_bf(v[u][e]);
-        }
-    }
-    for (; m < M; m += kColsumGroups) {
-      const u32x4_t v = ldg16(col + static_cast<size_t>(m) * N);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        s[2 * e] += lo_bf(v[e]);
-        s[2 * e + 1] += hi_bf(v[e]);
+      for (int i = 0; i < FM; ++i) {
+        const float tot = dbacc[i] + __shfl_xor(dbacc[i], 32, kWave);
+        const int row = m0 + wm * WTM + i * 32 + (lane & 31);
+        if (lane < 32 && row < p.M) p.db[row] = p.accumulate ? p.db[row] + tot : tot;
       }
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < 8; ++e) red[grp][chunk * 8 + e] = s[e];
-  __syncthreads();
-  if (threadIdx.x < kColsumCols) {
-    const int col = blockIdx.x * kColsumCols + threadIdx.x;
-    float t = 0.f;
-#pragma unroll 8
-    for (int g = 0; g < kColsumGroups; ++g) t += red[g][threadIdx.x];
-    if (col < N) {
-      if (accumulate) t += db[col];
-      db[col] = t;
     }
   }
 }
@@ -748,14 +726,8 @@ bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s) {
 }
 
 bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s) {
-  if (launch_lds<true, true, Epi::kF32>(a, s)) {
-    // bias gradient: column sums of dY (stored [tokens][a.M]) in a separate pass
-    if (a.db)
-      hipLaunchKernelGGL(colsum_kernel, dim3((a.M + kColsumCols - 1) / kColsumCols), dim3(256), 0, s, a.K, a.M, a.A,
-                         a.db, a.accumulate);
-    return true;
-  }
-  return launch_any<true, true, Epi::kF32>(a, s);
+  // both paths fuse the bias gradient into the weight-gradient kernel
+  return launch_lds<true, true, Epi::kF32>(a, s) || launch_any<true, true, Epi::kF32>(a, s);
 }
 
 }  // namespace optimus
