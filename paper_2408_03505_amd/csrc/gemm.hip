@@ -115,6 +115,104 @@ __device__ __forceinline__ void store_tile(const GemmArgs &p, const f32x16_t (&a
 
 }
 
+// Epilogue through LDS (direct-to-LDS kernels; the k-loop's buffers are free
+// by then).  The tile is written out in chunks of 64 rows: the waves owning a
+// chunk store their fp32 results (bias added) into LDS, row-major with a
+// 16-byte row pad (conflict-free for the 64-bank LDS), then every thread
+// streams whole rows out with 16-byte accesses, applying the residual, GELU,
+// GELU' or the fp32 accumulation on the way.  Output rows are written in full
+// 128-byte lines instead of 8-byte pieces scattered over 32 rows.
+constexpr int kEpiRows = 64;
+
+template <Epi EPI, int BM, int BN, int WM, int WN>
+__device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t (&acc)[BM / WM / 32][BN / WN / 32],
+                                               int m0, int n0, int wm, int wn, int lane, float *lds) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 32, FN = WTN / 32;
+  constexpr int LDR = BN + 4;  // floats per LDS row (16-byte pad)
+  static_assert(BM % kEpiRows == 0 && kEpiRows % 32 == 0, "epilogue chunking");
+  const int tid = threadIdx.x;
+  const int lrow = lane & 31;
+#pragma unroll 1
+  for (int c = 0; c < BM / kEpiRows; ++c) {
+    __syncthreads();  // LDS free (k-loop reads or the previous chunk's readers done)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r0 = wm * WTM + i * 32;  // fragment's first tile row
+      if (r0 < c * kEpiRows || r0 >= (c + 1) * kEpiRows) continue;
+      const int rl = r0 - c * kEpiRows + lrow;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int cl = wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+          f32x4_t v{acc[i][j][q * 4], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]};
+          if constexpr (EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu) {
+            const int nb = n0 + cl;
+            if (nb < p.N) {
+              const u32x2_t bw = *reinterpret_cast<const u32x2_t *>(p.bias + nb);
+              v[0] += lo_bf(bw[0]);
+              v[1] += hi_bf(bw[0]);
+              v[2] += lo_bf(bw[1]);
+              v[3] += hi_bf(bw[1]);
+            }
+          }
+          *reinterpret_cast<f32x4_t *>(lds + rl * LDR + cl) = v;
+        }
+      }
+    }
+    __syncthreads();
+    if constexpr (EPI == Epi::kF32) {
+      constexpr int PER_ROW = BN / 4;
+      for (int it = tid; it < kEpiRows * PER_ROW; it += NT) {
+        const int r = it / PER_ROW, cc = (it % PER_ROW) * 4;
+        const int gm = m0 + c * kEpiRows + r, gn = n0 + cc;
+        if (gm >= p.M || gn >= p.N) continue;
+        f32x4_t v = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc);
+        const size_t off = static_cast<size_t>(gm) * p.ldy + gn;
+        if (p.accumulate) v += *reinterpret_cast<const f32x4_t *>(p.Wf + off);
+        *reinterpret_cast<f32x4_t *>(p.Wf + off) = v;
+      }
+    } else {
+      constexpr int PER_ROW = BN / 8;
+      for (int it = tid; it < kEpiRows * PER_ROW; it += NT) {
+        const int r = it / PER_ROW, cc = (it % PER_ROW) * 8;
+        const int gm = m0 + c * kEpiRows + r, gn = n0 + cc;
+        if (gm >= p.M || gn >= p.N) continue;
+        const f32x4_t a = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc);
+        const f32x4_t b = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc + 4);
+        float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+        const size_t off = static_cast<size_t>(gm) * p.ldy + gn;
+        if constexpr (EPI == Epi::kBiasResid) {
+          const u32x4_t rw = ldg16(p.R + off);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += lo_bf(rw[e]);
+            v[2 * e + 1] += hi_bf(rw[e]);
+          }
+        }
+        if constexpr (EPI == Epi::kGeluGrad) {
+          const u32x4_t uw = ldg16(p.R + off);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] *= gelu_grad_f(lo_bf(uw[e]));
+            v[2 * e + 1] *= gelu_grad_f(hi_bf(uw[e]));
+          }
+        }
+        u32x4_t o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = pack2(v[2 * e], v[2 * e + 1]);
+        stg16(p.Y + off, o);
+        if constexpr (EPI == Epi::kBiasGelu) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = pack2(gelu_f(v[2 * e]), gelu_f(v[2 * e + 1]));
+          stg16(p.Y2 + off, o);
+        }
+      }
+    }
+  }
+}
+
 // Global -> register -> LDS staging of one [ROWS x BK] operand tile.
 template <int ROWS, int BK, int NT, bool TRANS>
 struct TileLoader;
@@ -629,7 +727,7 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       for (int j = 0; j < FN; ++j) bfr[0][j] = bfr[1][j];
     }
   }
-  store_tile<EPI, FM, FN, WTM, WTN>(p, acc, m0, n0, wm, wn, lane);
+  store_tile_lds<EPI, BM, BN, WM, WN>(p, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
   if constexpr (kDb) {
     if (do_db) {
       // lane l and l ^ 32 hold the two token halves of row (l % 32)
@@ -672,6 +770,159 @@ bool launch_any(const GemmArgs &a, hipStream_t s) {
   const long big = static_cast<long>((a.M + 255) / 256) * ((a.N + 127) / 128);
   if (big >= 512) return launch_cfg<256, 128, 64, 2, 2, AT, BT, EPI>(a, s);
   return launch_cfg<128, 128, 64, 2, 2, AT, BT, EPI>(a, s);
+}
+
+// ---------------------------------------------------------------------------
+// Ping-pong variant: 8 waves, two per SIMD (waves w and w + 4), in two groups
+// offset by one phase.  Each k-step has a load phase (issue this wave's share
+// of the DMA STAGES-1 k-steps ahead, read all of this k-step's fragments into
+// registers, wait for them) and a compute phase (the k-step's MFMAs, operands
+// already in registers); a workgroup barrier ends every phase.  While one
+// group computes, the other loads, so each SIMD's MFMA pipe is fed by one of
+// its two waves at a time.
+//
+// Buffer safety: k-step t is read by group 0 in phase 2t and by group 1 in
+// phase 2t+1; its buffer is refilled (k-step t+STAGES) from phase 2t+2 on.
+// Each wave waits for its own share of k-step t+1 in its load phase of t, so
+// both groups' shares have landed by the barrier that ends phase 2t+1.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
+__global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uint32_t a_bytes, uint32_t b_bytes) {
+  constexpr int NW = WM * WN;
+  static_assert(NW == 8, "ping-pong needs two waves per SIMD");
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int KS = BK / 16;
+  constexpr int A_BYTES = DirectLoader<BM, BK, NW, AT>::BYTES, B_BYTES = DirectLoader<BN, BK, NW, BT>::BYTES;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  static_assert(STAGES >= 3 && BK % 16 == 0, "pipeline shape");
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
+  const lds_char *smem = (const lds_char *)(smem_raw);  // generic -> LDS address space
+
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int grp = wid >> 2;                                          // 0: waves 0-3, 1: waves 4-7
+  const int wm = wid / WN, wn = wid % WN;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  DirectLoader<BM, BK, NW, AT> la;
+  DirectLoader<BN, BK, NW, BT> lb;
+  la.init(p.A, a_bytes, p.lda, m0, wid, lane);
+  lb.init(p.B, b_bytes, p.ldb, n0, wid, lane);
+  const uint32_t a_step = AT ? static_cast<uint32_t>(BK) * p.lda * 2 : BK * 2;
+  const uint32_t b_step = BT ? static_cast<uint32_t>(BK) * p.ldb * 2 : BK * 2;
+  FragAddr<BM, BK, FM, AT> fa;
+  FragAddr<BN, BK, FN, BT> fb;
+  fa.init(wm * WTM, lane);
+  fb.init(wn * WTN, lane);
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+  constexpr bool kDb = (EPI == Epi::kF32);
+  const bool do_db = kDb && p.db != nullptr && tn == 0 && wn == 0;
+  float dbacc[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) dbacc[i] = 0.f;
+
+  const int nk = (p.K + BK - 1) / BK;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+  constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s) {
+    if (s < nk) {
+      la.issue(lds0 + s * STAGE, s * a_step, wid);
+      lb.issue(lds0 + s * STAGE + A_BYTES, s * b_step, wid);
+    }
+  }
+  // k-step 0 resident for every wave
+  if (STAGES - 1 < nk)
+    wait_vmcnt<PER_STAGE * (STAGES - 2)>();
+  else
+    wait_vmcnt<0>();
+  auto barrier = [] {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  barrier();
+  if (grp == 1) barrier();  // group 1 runs one phase behind
+
+  bf16x8_t af[KS][FM], bfr[KS][FN];
+  for (int t = 0; t < nk; ++t) {
+    // ---- load phase
+    const int tl = t + STAGES - 1;
+    if (tl < nk) {
+      const uint32_t st = lds0 + (tl % STAGES) * STAGE;
+      la.issue(st, tl * a_step, wid);
+      lb.issue(st + A_BYTES, tl * b_step, wid);
+    }
+    const lds_char *As = smem + (t % STAGES) * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[kk][i] = fa.get(As, i, kk);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[kk][j] = fb.get(As + A_BYTES, j, kk);
+    }
+    // own share of k-step t+1 landed (k-steps t+2.. may still be in flight)
+    if (t + STAGES - 1 < nk)
+      wait_vmcnt<PER_STAGE * (STAGES - 2), 0>();
+    else
+      wait_vmcnt<0, 0>();
+    barrier();
+    // ---- compute phase
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[kk][j], af[kk][i], acc[i][j]);
+      if constexpr (kDb) {
+        if (do_db) {
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const u32x4_t w = __builtin_bit_cast(u32x4_t, af[kk][i]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dbacc[i] += lo_bf(w[e]) + hi_bf(w[e]);
+          }
+        }
+      }
+    }
+    barrier();
+  }
+  if (grp == 0) barrier();  // match group 1's extra barrier
+
+  store_tile_lds<EPI, BM, BN, WM, WN>(p, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
+  if constexpr (kDb) {
+    if (do_db) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const float tot = dbacc[i] + __shfl_xor(dbacc[i], 32, kWave);
+        const int row = m0 + wm * WTM + i * 32 + (lane & 31);
+        if (lane < 32 && row < p.M) p.db[row] = p.accumulate ? p.db[row] + tot : tot;
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
+bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
+  constexpr int NW = WM * WN;
+  constexpr size_t lds = static_cast<size_t>(STAGES) *
+                         (DirectLoader<BM, BK, NW, AT>::BYTES + DirectLoader<BN, BK, NW, BT>::BYTES);
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, BK, WM, WN, STAGES, AT, BT, EPI>), dim3(tiles), dim3(NW * 64), lds, s, a,
+                     a_bytes, b_bytes);
+  return true;
 }
 
 // Direct-to-LDS path: pick the tile that minimises (rounds of 256 CUs) x
