@@ -927,9 +927,11 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 
 // Direct-to-LDS path: pick the tile that minimises (rounds of 256 CUs) x
 // (tile area / per-tile efficiency).  Measured on MI355X at the ViT-22B layer
-// shapes: 8-wave 256x256 tiles are the most efficient per tile, 8-wave
-// 256x192 tiles divide the 6144-wide and 18432-wide outputs into whole
-// rounds, and 4-wave 128x128 tiles serve small problems.
+// shapes with random bf16 data: 256x256 tiles are the most efficient per
+// tile, 256x192 tiles divide the 6144- and 18432-wide outputs into whole
+// rounds, 128x128 tiles serve small problems.  Kernels whose B operand is
+// contraction-strided (input and weight gradients) run the ping-pong
+// schedule (BK = 32, 4 stages), which hides their transpose reads better.
 // Returns false when the operands do not fit the path's constraints.
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s) {
@@ -947,8 +949,14 @@ bool launch_lds(const GemmArgs &a, hipStream_t s) {
   };
   const double cL = cost(256, 256, 1.0), cM = cost(256, 192, 0.95), cS = cost(128, 128, 0.75);
   const uint32_t ab = static_cast<uint32_t>(a_bytes), bb = static_cast<uint32_t>(b_bytes);
-  if (cL <= cM && cL <= cS) return launch_lds_cfg<256, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);
-  if (cM <= cS) return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
+  if (cL <= cM && cL <= cS) {
+    if constexpr (BT) return launch_pp_cfg<256, 256, 32, 2, 4, 4, AT, BT, EPI>(a, ab, bb, s);
+    return launch_lds_cfg<256, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);
+  }
+  if (cM <= cS) {
+    if constexpr (AT && BT) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+    return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
+  }
   return launch_lds_cfg<128, 128, BK, 2, 2, 2, AT, BT, EPI>(a, ab, bb, s);
 }
 
