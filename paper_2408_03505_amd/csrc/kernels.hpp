@@ -14,7 +14,6 @@ typedef uint16_t bf16_t;
 // ---- LayerNorm
 bool launch_ln_fwd(int rows, int cols, const bf16_t *x, const bf16_t *gamma, const bf16_t *beta, float eps,
                    bf16_t *y, float *mean, float *rstd, hipStream_t s);
-int ln_bwd_blocks(int rows);
 size_t ln_bwd_ws_bytes(int rows, int cols);
 bool launch_ln_bwd(int rows, int cols, const bf16_t *dy, const bf16_t *x, const float *mean, const float *rstd,
                    const bf16_t *gamma, const bf16_t *dresid, bf16_t *dx, float *dgamma, float *dbeta,
