@@ -7,13 +7,12 @@
 // orientation: the forward computes S^T = K Q^T, so each lane of the 32x32
 // result owns one query and holds that query's logits for 16 keys.  The row
 // max and row sum of the online softmax are then in-lane reductions plus one
-// exchange with lane^32, and the exponentiated tile is already laid out as
-// the B operand of O^T += V^T P^T once the key order inside each 16-key step
-// is permuted the same way in both operands (lane half h holds keys
-// 4h..4h+3 and 8+4h..8+4h+3).  V^T is staged in LDS as [d][key] through an
-// 8x8 register transpose, so the A operand is two 8-byte LDS reads.  Head
-// dims 64, 80 and 128 contract in 16-wide steps; the O^T rows are padded to
-// a multiple of 32 (80 -> 96) and the padding rows are never stored.
+// exchange with lane^32, and the exponentiated tile is already the B operand
+// of O^T += V^T P^T.  Token tiles of K, V (forward, dQ) or Q, dO (dK/dV) go
+// HBM -> LDS by DMA, double-buffered, and the token-contracting products read
+// their A operand with the LDS transpose read.  Head dims 64, 80 and 128
+// contract in 16-wide steps; d-major results are padded to a multiple of 32
+// rows (80 -> 96) and the padding rows are never stored.
 //
 // The backward is two kernels and uses no atomics: one per query tile that
 // recomputes P^T and dP^T and accumulates dQ^T = K^T dS^T over all keys (and
@@ -23,6 +22,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "lds_dma.hpp"
 
 namespace optimus {
 
@@ -36,19 +36,7 @@ template <int D>
 struct Head {
   static constexpr int KS = D / 16;              // 16-wide contraction steps over d
   static constexpr int NF = (D + 31) / 32;       // 32-row fragments of a d-major result
-  static constexpr int DP = NF * 32;             // padded d rows
-  static constexpr int LDR = D + 8;              // LDS row stride of [token][d] tiles
-  static constexpr int LDT = kKT + 8;            // LDS row stride of [d][token] tiles
 };
-
-__device__ __forceinline__ bf16x8_t lds_b128(const bf16_t *p) { return *reinterpret_cast<const bf16x8_t *>(p); }
-
-// Two 8-byte LDS reads forming one MFMA operand in the permuted key order.
-__device__ __forceinline__ bf16x8_t lds_perm(const bf16_t *row, int step, int hf) {
-  const u32x2_t a = *reinterpret_cast<const u32x2_t *>(row + step * 16 + 4 * hf);
-  const u32x2_t b = *reinterpret_cast<const u32x2_t *>(row + step * 16 + 8 + 4 * hf);
-  return as_bf16x8(u32x4_t{a[0], a[1], b[0], b[1]});
-}
 
 // Pack eight fp32 (registers 8*half .. 8*half+7 of a 32x32 result) to bf16.
 __device__ __forceinline__ bf16x8_t pack8(const f32x16_t &v, int half) {
@@ -56,37 +44,6 @@ __device__ __forceinline__ bf16x8_t pack8(const f32x16_t &v, int half) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) r[e] = pack2(v[8 * half + 2 * e], v[8 * half + 2 * e + 1]);
   return as_bf16x8(r);
-}
-
-// Row-major [kKT][D] tile of tokens t0.. (rows >= S zero-filled).
-template <int D>
-__device__ __forceinline__ void stage_rows(bf16_t *dst, const bf16_t *src, int ld, int t0, int S, int tid) {
-  constexpr int C = D / 8;
-  for (int c = tid; c < kKT * C; c += 256) {
-    const int t = c / C, dc = c % C;
-    u32x4_t v{0u, 0u, 0u, 0u};
-    if (t0 + t < S) v = ldg16(src + static_cast<size_t>(t0 + t) * ld + dc * 8);
-    *reinterpret_cast<u32x4_t *>(dst + t * Head<D>::LDR + dc * 8) = v;
-  }
-}
-
-// Transposed [D][kKT] tile (d-major, tokens contiguous) via 8x8 register blocks.
-template <int D>
-__device__ __forceinline__ void stage_cols(bf16_t *dst, const bf16_t *src, int ld, int t0, int S, int tid) {
-  constexpr int NB = (kKT / 8) * (D / 8);
-  if (tid < NB) {
-    const int tb = tid % (kKT / 8), db = tid / (kKT / 8);
-    u32x4_t in[8], out[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int t = t0 + tb * 8 + j;
-      in[j] = (t < S) ? ldg16(src + static_cast<size_t>(t) * ld + db * 8) : u32x4_t{0u, 0u, 0u, 0u};
-    }
-    transpose8x8(in, out);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4_t *>(dst + (db * 8 + i) * Head<D>::LDT + tb * 8) = out[i];
-  }
 }
 
 // Load this lane's token row (d values 16*kk + 8*hf .. +7 for each step kk)
@@ -116,25 +73,118 @@ __device__ __forceinline__ void store_dmajor(bf16_t *dst, const f32x16_t (&acc)[
 }
 
 // ------------------------------------------------------------------ forward
+//
+// K and V tiles of 64 tokens go HBM -> LDS by DMA (double-buffered, no
+// staging registers), rows of kDL = 128 columns taken from the head's first
+// column (columns past head_dim belong to the neighbouring data and are
+// never contracted; rows past the sequence belong to the next sequence or
+// read as zero past the tensor, and are masked out of the softmax).  K is
+// read as the A operand of S^T = K Q^T with ds_read_b128; V is read as the A
+// operand of O^T += V^T P^T with ds_read_b64_tr_b16.  The transpose read
+// delivers tokens in natural order while the P^T registers hold them with
+// bits 2 and 3 of the token index swapped, so V rows are stored with that
+// swap (perm23).  One XOR swizzle serves both read patterns: chunk c of tile
+// row r sits at c ^ tsw(r), distinct over any 16 consecutive rows (the
+// ds_read_b128 pattern) and spreading any 4 consecutive rows over disjoint
+// 64-byte ranges (the transpose-read pattern).
+
+constexpr int kDL = 128;                    // LDS row length (elements)
+constexpr int kTileBytes = kKT * kDL * 2;   // one 64-token tile: 16 KB
+
+__device__ __forceinline__ int tsw(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int tile_off(int r, int c) { return r * (kDL * 2) + ((c ^ tsw(r)) << 4); }
+__device__ __forceinline__ int perm23(int r) { return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+// Per-lane byte offsets of this wave's DMA loads of one tile (16 loads of
+// 1 KB per tile, split over NW waves; tile-relative: the tile's first row and
+// column go in the scalar offset).  perm stores token perm23(r) in row r.
+template <int NW>
+__device__ __forceinline__ void tile_voff(uint32_t (&v)[16 / NW], int wid, int lane, int ld, bool perm) {
+#pragma unroll
+  for (int i = 0; i < 16 / NW; ++i) {
+    const int o = (wid * (16 / NW) + i) * 1024 + lane * 16;
+    const int pr = o >> 8, c = ((o & 255) >> 4) ^ tsw(pr);
+    v[i] = static_cast<uint32_t>(((perm ? perm23(pr) : pr) * ld + c * 8) * 2);
+  }
+}
+
+// Issue one tile's DMA loads.  In the last tile of a sequence (rem < kKT
+// rows left) the rows past the sequence re-read the tile's first row: every
+// product with those rows carries a zero weight, but a non-finite value in
+// the next sequence would still turn that zero into NaN.
+template <int NW>
+__device__ __forceinline__ void tile_issue(const u32x4_t &rsrc, uint32_t lds_tile, const uint32_t (&voff)[16 / NW],
+                                           uint32_t soff, int wid, int lane, int rem, int ld, bool perm) {
+  const uint32_t sl = __builtin_amdgcn_readfirstlane(soff);
+  if (rem >= kKT) {
+#pragma unroll
+    for (int i = 0; i < 16 / NW; ++i)
+      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * (16 / NW) + i) * 1024), voff[i], sl);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16 / NW; ++i) {
+      const int pr = (wid * (16 / NW) + i) * 4 + (lane >> 4);
+      const int tok = perm ? perm23(pr) : pr;
+      const uint32_t v = tok < rem ? voff[i] : voff[i] - static_cast<uint32_t>(tok * ld * 2);
+      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * (16 / NW) + i) * 1024), v, sl);
+    }
+  }
+}
+
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// MFMA A operand (rows = tile rows rbase.., contraction = columns 16kk..) by ds_read_b128.
+__device__ __forceinline__ bf16x8_t tile_rows(const lds_char *t, int rbase, int kk, int lane) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t *>(
+      t + tile_off(rbase + (lane & 31), kk * 2 + (lane >> 5)));
+}
+
+// MFMA A operand (rows = columns nbase.., contraction = tile rows 16st..) by
+// two ds_read_b64_tr_b16.
+__device__ __forceinline__ bf16x8_t tile_cols(const lds_char *t, int nbase, int st, int lane) {
+  const int k = st * 16 + 8 * (lane >> 5) + ((lane & 15) >> 2);
+  const int n = nbase + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int in = (n & 7) * 2;
+  return lds_read_tr(t + tile_off(k, n >> 3) + in, t + tile_off(k + 4, n >> 3) + in);
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
-                                                       bf16_t *__restrict__ o, float *__restrict__ lse) {
+                                                       uint32_t qkv_bytes, bf16_t *__restrict__ o,
+                                                       float *__restrict__ lse) {
   using H = Head<D>;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[kKT * H::LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[H::DP * H::LDT];
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];  // 2 x (K tile, V tile)
+  const lds_char *smem = (const lds_char *)(smem_raw);
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
   const int nqt = (S + kRows - 1) / kRows;
   const int qt = blockIdx.x % nqt;
   const int bh = blockIdx.x / nqt;
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, hf = lane >> 5;
+  const int lane = threadIdx.x & 63, hf = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q = qt * kRows + wid * 32 + (lane & 31);
   const bool qvalid = q < S;
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
-  const bf16_t *kbase = base + A + h * D;
-  const bf16_t *vbase = base + 2 * A + h * D;
+
+  const u32x4_t rsrc = make_rsrc(qkv, qkv_bytes);
+  uint32_t voff_k[4], voff_v[4];
+  tile_voff<4>(voff_k, wid, lane, ld, false);
+  tile_voff<4>(voff_v, wid, lane, ld, true);
+  const uint32_t k_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + A + h * D) * 2);
+  const uint32_t v_base = k_base + static_cast<uint32_t>(A * 2);
+  const uint32_t tile_step = static_cast<uint32_t>(kKT * ld * 2);
+  auto issue = [&](int t) {
+    const uint32_t buf = lds0 + (t & 1) * 2 * kTileBytes;
+    const int rem = S - t * kKT;
+    tile_issue<4>(rsrc, buf, voff_k, k_base + t * tile_step, wid, lane, rem, ld, false);
+    tile_issue<4>(rsrc, buf + kTileBytes, voff_v, v_base + t * tile_step, wid, lane, rem, ld, true);
+  };
 
   bf16x8_t qf[H::KS];
   load_row_operand<D>(qf, base + static_cast<size_t>(q) * ld + h * D, qvalid, hf);
@@ -145,19 +195,26 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
   float m = -INFINITY, l = 0.f;
   const float c = kLog2e / sqrtf(static_cast<float>(D));
 
-  for (int k0 = 0; k0 < S; k0 += kKT) {
-    __syncthreads();
-    stage_rows<D>(Ks, kbase, ld, k0, S, tid);
-    stage_cols<D>(Vt, vbase, ld, k0, S, tid);
-    __syncthreads();
+  const int nk = (S + kKT - 1) / kKT;
+  issue(0);
+  for (int t = 0; t < nk; ++t) {
+    if (t + 1 < nk) {
+      issue(t + 1);
+      wait_vmcnt<8>();  // this wave's 8 loads of tile t+1 may stay in flight
+    } else {
+      wait_vmcnt<0>();
+    }
+    block_barrier();
+    const lds_char *Ks = smem + (t & 1) * 2 * kTileBytes;
+    const lds_char *Vs = Ks + kTileBytes;
+    const int k0 = t * kKT;
 
     f32x16_t s[2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       s[f] = f32x16_t{};
 #pragma unroll
-      for (int kk = 0; kk < H::KS; ++kk)
-        s[f] = mfma32(lds_b128(Ks + (f * 32 + (lane & 31)) * H::LDR + kk * 16 + hf * 8), qf[kk], s[f]);
+      for (int kk = 0; kk < H::KS; ++kk) s[f] = mfma32(tile_rows(Ks, f * 32, kk, lane), qf[kk], s[f]);
     }
     float mt = m;
 #pragma unroll
@@ -177,9 +234,9 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(s[f][i] - mt);
-        s[f][i] = p;
-        ls += p;
+        const float pv = exp2f(s[f][i] - mt);
+        s[f][i] = pv;
+        ls += pv;
       }
     l = l * alpha + ls;
 #pragma unroll
@@ -188,9 +245,9 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
     for (int st = 0; st < kKT / 16; ++st) {
       const bf16x8_t pb = pack8(s[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf)
-        acc[nf] = mfma32(lds_perm(Vt + (nf * 32 + (lane & 31)) * H::LDT, st, hf), pb, acc[nf]);
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Vs, nf * 32, st, lane), pb, acc[nf]);
     }
+    block_barrier();  // every wave is done with this buffer before it is refilled
   }
 
   const float lt = l + __shfl_xor(l, 32, kWave);
@@ -201,36 +258,56 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
 }
 
 // ------------------------------------------------------------------ backward: dQ and D
+//
+// Per query tile: S^T = K Q^T and dP^T = V dO^T use K and V tiles stored with
+// permuted rows (perm23) and read by ds_read_b128, so the dS^T registers hold
+// keys in natural order per transpose-read position; dQ^T += K^T dS^T then
+// reads a second, natural-order copy of the K tile with ds_read_b64_tr_b16.
+// This kernel also writes D_i = dO_i . O_i for the dK/dV kernel.
 
-template <int D>
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
-                                                          const bf16_t *__restrict__ o, const float *__restrict__ lse,
-                                                          const bf16_t *__restrict__ dO, bf16_t *__restrict__ dqkv,
-                                                          float *__restrict__ dvec) {
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
+                                                              uint32_t qkv_bytes, const bf16_t *__restrict__ o,
+                                                              const float *__restrict__ lse,
+                                                              const bf16_t *__restrict__ dO, bf16_t *__restrict__ dqkv,
+                                                              float *__restrict__ dvec) {
   using H = Head<D>;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[kKT * H::LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[kKT * H::LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[H::DP * H::LDT];
+  constexpr int ROWS = 32 * NW, STAGE = 3 * kTileBytes;  // Kp, Vp, Kn
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
+  const lds_char *smem = (const lds_char *)(smem_raw);
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
-  const int nqt = (S + kRows - 1) / kRows;
+  const int nqt = (S + ROWS - 1) / ROWS;
   const int qt = blockIdx.x % nqt;
   const int bh = blockIdx.x / nqt;
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, hf = lane >> 5;
-  const int q = qt * kRows + wid * 32 + (lane & 31);
+  const int lane = threadIdx.x & 63, hf = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q = qt * ROWS + wid * 32 + (lane & 31);
   const bool qvalid = q < S;
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
-  const bf16_t *kbase = base + A + h * D;
-  const bf16_t *vbase = base + 2 * A + h * D;
   const size_t orow = (static_cast<size_t>(b) * S + q) * A + h * D;
+
+  const u32x4_t rsrc = make_rsrc(qkv, qkv_bytes);
+  uint32_t voff_p[16 / NW], voff_n[16 / NW];
+  tile_voff<NW>(voff_p, wid, lane, ld, true);
+  tile_voff<NW>(voff_n, wid, lane, ld, false);
+  const uint32_t k_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + A + h * D) * 2);
+  const uint32_t v_base = k_base + static_cast<uint32_t>(A * 2);
+  const uint32_t tile_step = static_cast<uint32_t>(kKT * ld * 2);
+  auto issue = [&](int t) {
+    const uint32_t buf = lds0 + (t & 1) * STAGE;
+    const int rem = S - t * kKT;
+    tile_issue<NW>(rsrc, buf, voff_p, k_base + t * tile_step, wid, lane, rem, ld, true);
+    tile_issue<NW>(rsrc, buf + kTileBytes, voff_p, v_base + t * tile_step, wid, lane, rem, ld, true);
+    tile_issue<NW>(rsrc, buf + 2 * kTileBytes, voff_n, k_base + t * tile_step, wid, lane, rem, ld, false);
+  };
 
   bf16x8_t qf[H::KS], df[H::KS];
   load_row_operand<D>(qf, base + static_cast<size_t>(q) * ld + h * D, qvalid, hf);
   load_row_operand<D>(df, dO + orow, qvalid, hf);
-
-  // D_i = dO_i . O_i (this lane holds half of the d values of its query)
-  float dd = 0.f;
+  float dd = 0.f;  // D_i (this lane holds half of the d values of its query)
   if (qvalid) {
 #pragma unroll
     for (int kk = 0; kk < H::KS; ++kk) {
@@ -248,40 +325,45 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(int B, int S, int head
   f32x16_t acc[H::NF];
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
-
-  for (int k0 = 0; k0 < S; k0 += kKT) {
-    __syncthreads();
-    stage_rows<D>(Ks, kbase, ld, k0, S, tid);
-    stage_rows<D>(Vs, vbase, ld, k0, S, tid);
-    stage_cols<D>(Kt, kbase, ld, k0, S, tid);
-    __syncthreads();
-
-    f32x16_t s[2], dp[2];
+  constexpr int LOADS = 3 * (16 / NW);
+  const int nk = (S + kKT - 1) / kKT;
+  issue(0);
+  for (int t = 0; t < nk; ++t) {
+    if (t + 1 < nk) {
+      issue(t + 1);
+      wait_vmcnt<LOADS>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    block_barrier();
+    const lds_char *Kp = smem + (t & 1) * STAGE, *Vp = Kp + kTileBytes, *Kn = Kp + 2 * kTileBytes;
+    const int k0 = t * kKT;
+    f32x16_t sv[2], dp[2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
-      s[f] = f32x16_t{};
+      sv[f] = f32x16_t{};
       dp[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) {
-        s[f] = mfma32(lds_b128(Ks + (f * 32 + (lane & 31)) * H::LDR + kk * 16 + hf * 8), qf[kk], s[f]);
-        dp[f] = mfma32(lds_b128(Vs + (f * 32 + (lane & 31)) * H::LDR + kk * 16 + hf * 8), df[kk], dp[f]);
+        sv[f] = mfma32(tile_rows(Kp, f * 32, kk, lane), qf[kk], sv[f]);
+        dp[f] = mfma32(tile_rows(Vp, f * 32, kk, lane), df[kk], dp[f]);
       }
     }
+    // register i of fragment f is key k0 + perm23(f*32 + 8(i/4) + 4 hf + i%4)
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-        const float p = (key < S) ? exp2f(s[f][i] * c - lse2) : 0.f;
-        s[f][i] = p * (dp[f][i] - dd);  // dS^T
+        const int key = k0 + perm23(f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3));
+        sv[f][i] = (key < S) ? exp2f(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
       }
 #pragma unroll
     for (int st = 0; st < kKT / 16; ++st) {
-      const bf16x8_t pb = pack8(s[st >> 1], st & 1);
+      const bf16x8_t sb = pack8(sv[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf)
-        acc[nf] = mfma32(lds_perm(Kt + (nf * 32 + (lane & 31)) * H::LDT, st, hf), pb, acc[nf]);
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Kn, nf * 32, st, lane), sb, acc[nf]);
     }
+    block_barrier();
   }
   if (qvalid)
     store_dmajor<D>(dqkv + (static_cast<size_t>(b) * S + q) * ld + h * D, acc, 1.0f / sqrtf(static_cast<float>(D)),
@@ -289,32 +371,61 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(int B, int S, int head
 }
 
 // ------------------------------------------------------------------ backward: dK, dV
+//
+// Per key tile: S = Q K^T and dP = dO V^T use Q and dO tiles with permuted
+// rows (ds_read_b128); dV^T += dO^T P and dK^T += Q^T dS read natural-order
+// copies of dO and Q with ds_read_b64_tr_b16.  lse and D of the tile's
+// queries come in by DMA as well; queries past the sequence are masked out.
 
-template <int D>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
-                                                            const float *__restrict__ lse,
-                                                            const bf16_t *__restrict__ dO,
-                                                            const float *__restrict__ dvec,
-                                                            bf16_t *__restrict__ dqkv) {
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, int heads,
+                                                                const bf16_t *__restrict__ qkv, uint32_t qkv_bytes,
+                                                                const float *__restrict__ lse,
+                                                                const bf16_t *__restrict__ dO, uint32_t do_bytes,
+                                                                const float *__restrict__ dvec,
+                                                                bf16_t *__restrict__ dqkv) {
   using H = Head<D>;
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[kKT * H::LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t Ds[kKT * H::LDR];
-  __shared__ __attribute__((aligned(16))) bf16_t Qt[H::DP * H::LDT];
-  __shared__ __attribute__((aligned(16))) bf16_t Dt[H::DP * H::LDT];
-  __shared__ __attribute__((aligned(16))) float Ls[kKT];
-  __shared__ __attribute__((aligned(16))) float Dv[kKT];
+  constexpr int ROWS = 32 * NW, TILES = 4 * kTileBytes;  // Qp, dOp, Qn, dOn
+  constexpr int STAGE = TILES + 2 * kKT * 4;             // + lse, D
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
+  const lds_char *smem = (const lds_char *)(smem_raw);
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
-  const int nkt = (S + kRows - 1) / kRows;
+  const int nkt = (S + ROWS - 1) / ROWS;
   const int kt = blockIdx.x % nkt;
   const int bh = blockIdx.x / nkt;
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, hf = lane >> 5;
-  const int key = kt * kRows + wid * 32 + (lane & 31);
+  const int lane = threadIdx.x & 63, hf = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int key = kt * ROWS + wid * 32 + (lane & 31);
   const bool kvalid = key < S;
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
-  const bf16_t *qbase = base + h * D;
-  const bf16_t *dobase = dO + static_cast<size_t>(b) * S * A + h * D;
+
+  const u32x4_t rq = make_rsrc(qkv, qkv_bytes), rd = make_rsrc(dO, do_bytes);
+  uint32_t vq_p[16 / NW], vq_n[16 / NW], vd_p[16 / NW], vd_n[16 / NW];
+  tile_voff<NW>(vq_p, wid, lane, ld, true);
+  tile_voff<NW>(vq_n, wid, lane, ld, false);
+  tile_voff<NW>(vd_p, wid, lane, A, true);
+  tile_voff<NW>(vd_n, wid, lane, A, false);
+  const uint32_t q_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + h * D) * 2);
+  const uint32_t d_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * A + h * D) * 2);
+  const uint32_t q_step = static_cast<uint32_t>(kKT * ld * 2), d_step = static_cast<uint32_t>(kKT * A * 2);
+  const uint32_t vec_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * heads * S * 4);
+  const u32x4_t rl = make_rsrc(lse, vec_bytes), rv = make_rsrc(dvec, vec_bytes);
+  auto issue = [&](int t) {
+    const uint32_t buf = lds0 + (t & 1) * STAGE;
+    const int rem = S - t * kKT;
+    tile_issue<NW>(rq, buf, vq_p, q_base + t * q_step, wid, lane, rem, ld, true);
+    tile_issue<NW>(rd, buf + kTileBytes, vd_p, d_base + t * d_step, wid, lane, rem, A, true);
+    tile_issue<NW>(rq, buf + 2 * kTileBytes, vq_n, q_base + t * q_step, wid, lane, rem, ld, false);
+    tile_issue<NW>(rd, buf + 3 * kTileBytes, vd_n, d_base + t * d_step, wid, lane, rem, A, false);
+    // lse (wave 0) and D (wave 1) of the tile's 64 queries; entries past the
+    // sequence are masked out of P below
+    const uint32_t vs = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((bh * S + t * kKT) * 4));
+    if (wid == 0) buffer_load_lds4(rl, __builtin_amdgcn_readfirstlane(buf + TILES), lane * 4, vs);
+    if (wid == 1) buffer_load_lds4(rv, __builtin_amdgcn_readfirstlane(buf + TILES + kKT * 4), lane * 4, vs);
+  };
 
   bf16x8_t kf[H::KS], vf[H::KS];
   load_row_operand<D>(kf, base + static_cast<size_t>(key) * ld + A + h * D, kvalid, hf);
@@ -324,57 +435,63 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(int B, int S, int he
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) dk[i] = dv[i] = f32x16_t{};
   const float c = kLog2e / sqrtf(static_cast<float>(D));
-
-  for (int q0 = 0; q0 < S; q0 += kKT) {
-    __syncthreads();
-    stage_rows<D>(Qs, qbase, ld, q0, S, tid);
-    stage_rows<D>(Ds, dobase, A, q0, S, tid);
-    stage_cols<D>(Qt, qbase, ld, q0, S, tid);
-    stage_cols<D>(Dt, dobase, A, q0, S, tid);
-    if (tid < kKT) {
-      const int qq = q0 + tid;
-      // queries past the end get lse = +inf (P = 0) and D = 0
-      Ls[tid] = (qq < S) ? lse[static_cast<size_t>(bh) * S + qq] * kLog2e : INFINITY;
-      Dv[tid] = (qq < S) ? dvec[static_cast<size_t>(bh) * S + qq] : 0.f;
+  constexpr int LOADS = 4 * (16 / NW);
+  const int nq = (S + kKT - 1) / kKT;
+  issue(0);
+  for (int t = 0; t < nq; ++t) {
+    if (t + 1 < nq) {
+      issue(t + 1);
+      if (wid < 2)
+        wait_vmcnt<LOADS + 1>();
+      else
+        wait_vmcnt<LOADS>();
+    } else {
+      wait_vmcnt<0>();
     }
-    __syncthreads();
-
-    f32x16_t s[2], dp[2];
+    block_barrier();
+    const lds_char *Qp = smem + (t & 1) * STAGE, *Dp = Qp + kTileBytes;
+    const lds_char *Qn = Qp + 2 * kTileBytes, *Dn = Qp + 3 * kTileBytes;
+    const float *Ls = reinterpret_cast<const float *>(smem_raw + (t & 1) * STAGE + TILES);
+    const int q0 = t * kKT;
+    f32x16_t sv[2], dp[2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
-      s[f] = f32x16_t{};
+      sv[f] = f32x16_t{};
       dp[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) {
-        s[f] = mfma32(lds_b128(Qs + (f * 32 + (lane & 31)) * H::LDR + kk * 16 + hf * 8), kf[kk], s[f]);
-        dp[f] = mfma32(lds_b128(Ds + (f * 32 + (lane & 31)) * H::LDR + kk * 16 + hf * 8), vf[kk], dp[f]);
+        sv[f] = mfma32(tile_rows(Qp, f * 32, kk, lane), kf[kk], sv[f]);
+        dp[f] = mfma32(tile_rows(Dp, f * 32, kk, lane), vf[kk], dp[f]);
       }
     }
-    // s[f][i] is query f*32 + 8*(i/4) + 4*hf + i%4 of this tile, key = this lane
+    // register 4g+e of fragment f is query perm23(f*32 + 8g + 4hf + e)
+    //   = f*32 + 16(g/2) + 8hf + 4(g%2) + e  (four consecutive queries)
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int qi = f * 32 + g * 8 + hf * 4;
-        const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi);
-        const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Dv + qi);
+        const int qi = f * 32 + 16 * (g >> 1) + 8 * hf + 4 * (g & 1);
+        const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi) * kLog2e;
+        const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + kKT + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = exp2f(s[f][4 * g + e] * c - l4[e]);
-          s[f][4 * g + e] = p;
-          dp[f][4 * g + e] = p * (dp[f][4 * g + e] - d4[e]);
+          const bool ok = q0 + qi + e < S;
+          const float pv = exp2f(sv[f][4 * g + e] * c - l4[e]);
+          sv[f][4 * g + e] = ok ? pv : 0.f;
+          dp[f][4 * g + e] = ok ? pv * (dp[f][4 * g + e] - d4[e]) : 0.f;
         }
       }
 #pragma unroll
     for (int st = 0; st < kKT / 16; ++st) {
-      const bf16x8_t pb = pack8(s[st >> 1], st & 1);
+      const bf16x8_t pb = pack8(sv[st >> 1], st & 1);
       const bf16x8_t sb = pack8(dp[st >> 1], st & 1);
 #pragma unroll
       for (int nf = 0; nf < H::NF; ++nf) {
-        dv[nf] = mfma32(lds_perm(Dt + (nf * 32 + (lane & 31)) * H::LDT, st, hf), pb, dv[nf]);
-        dk[nf] = mfma32(lds_perm(Qt + (nf * 32 + (lane & 31)) * H::LDT, st, hf), sb, dk[nf]);
+        dv[nf] = mfma32(tile_cols(Dn, nf * 32, st, lane), pb, dv[nf]);
+        dk[nf] = mfma32(tile_cols(Qn, nf * 32, st, lane), sb, dk[nf]);
       }
     }
+    block_barrier();  // every wave is done with this buffer before it is refilled
   }
   if (kvalid) {
     bf16_t *row = dqkv + (static_cast<size_t>(b) * S + key) * ld + h * D;
@@ -386,15 +503,31 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(int B, int S, int he
 template <int D>
 void launch_fwd_d(int B, int S, int heads, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
   const int blocks = B * heads * ((S + kRows - 1) / kRows);
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(blocks), dim3(256), 0, s, B, S, heads, qkv, o, lse);
+  const uint32_t bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * 3 * heads * D * 2);
+  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(blocks), dim3(256), 4 * kTileBytes, s, B, S, heads, qkv, bytes, o, lse);
 }
 
 template <int D>
 void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, const float *lse, const bf16_t *dO,
                   bf16_t *dqkv, float *dvec, hipStream_t s) {
-  const int blocks = B * heads * ((S + kRows - 1) / kRows);
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(blocks), dim3(256), 0, s, B, S, heads, qkv, o, lse, dO, dqkv, dvec);
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(blocks), dim3(256), 0, s, B, S, heads, qkv, lse, dO, dvec, dqkv);
+  constexpr int NWQ = 4, NWK = 4;
+  const uint32_t qkv_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * 3 * heads * D * 2);
+  const uint32_t do_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * heads * D * 2);
+  const int qblocks = B * heads * ((S + 32 * NWQ - 1) / (32 * NWQ));
+  const int kblocks = B * heads * ((S + 32 * NWK - 1) / (32 * NWK));
+  constexpr int kDqLds = 2 * 3 * kTileBytes, kDkvLds = 2 * (4 * kTileBytes + 2 * kKT * 4);
+  static const bool attrs_set = [] {
+    hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dq_kernel<D, NWQ>),
+                        hipFuncAttributeMaxDynamicSharedMemorySize, kDqLds);
+    hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D, NWK>),
+                        hipFuncAttributeMaxDynamicSharedMemorySize, kDkvLds);
+    return true;
+  }();
+  (void)attrs_set;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NWQ>), dim3(qblocks), dim3(NWQ * 64), kDqLds, s, B, S, heads,
+                     qkv, qkv_bytes, o, lse, dO, dqkv, dvec);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NWK>), dim3(kblocks), dim3(NWK * 64), kDkvLds, s, B, S, heads, qkv,
+                     qkv_bytes, lse, dO, do_bytes, dvec, dqkv);
 }
 
 }  // namespace
@@ -404,6 +537,9 @@ size_t attn_bwd_ws_bytes(int B, int S, int heads) {
 }
 
 bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
+  // every tile address (up to one tile past the tensor) must stay a 32-bit buffer offset
+  const uint64_t ld = 3ull * heads * d;
+  if ((static_cast<uint64_t>(B) * S + kKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
   switch (d) {
     case 64: launch_fwd_d<64>(B, S, heads, qkv, o, lse, s); return true;
     case 80: launch_fwd_d<80>(B, S, heads, qkv, o, lse, s); return true;
@@ -414,6 +550,8 @@ bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *
 
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s) {
+  const uint64_t ld = 3ull * heads * d;
+  if ((static_cast<uint64_t>(B) * S + kKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
   switch (d) {
     case 64: launch_bwd_d<64>(B, S, heads, qkv, o, lse, dO, dqkv, dvec, s); return true;
     case 80: launch_bwd_d<80>(B, S, heads, qkv, o, lse, dO, dqkv, dvec, s); return true;

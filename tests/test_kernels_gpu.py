@@ -320,3 +320,24 @@ def test_attn_bwd_is_deterministic():
     b = B.enc_attn_bwd(Bn, S, nh, d, qkv, o, lse, dO)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("S,d", [(100, 64), (197, 80), (70, 128), (256, 128)])
+def test_attn_sequences_are_independent(S, d):
+    """Tiles of the last keys of a sequence overhang into the next sequence;
+    non-finite values there must not leak into this sequence's results."""
+    announce(f"attn isolation S={S} d={d}")
+    Bn, nh = 2, 2
+    qkv = _attn_inputs(Bn, S, nh, d, 131, 1.0)
+    dO = random_bf16((Bn * S, nh * d), 132)
+    qkv[S:] = float("nan")
+    dO[S:] = float("inf")
+    o, lse = B.enc_attn_fwd(Bn, S, nh, d, cuda(qkv))
+    dqkv = B.enc_attn_bwd(Bn, S, nh, d, cuda(qkv), o, lse, cuda(dO))
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention_fwd(f64(qkv[:S]), 1, S, nh, d)
+    assert max_rel(f64(o[:S]), ro) < TOL_ACT
+    assert np.abs(f64(lse[:1]) - rl).max() < 2e-3 * max(1.0, np.abs(rl).max())
+    ref = oracle.attention_bwd(f64(qkv[:S]), f64(dO[:S]), 1, S, nh, d)
+    assert np.isfinite(f64(dqkv[:S])).all()
+    assert max_rel(f64(dqkv[:S]), ref) < TOL_GRAD
