@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured MFMA-only and device-copy reference kernels")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the timed region, run one device copy of this many MiB "
                          "(a known-size reference for the HBM byte counters)")
@@ -49,35 +51,87 @@ def parse():
     return ap.parse_args()
 
 
-# GPU dispatches of each chain entry, in launch order
-DISPATCHES = {"ln1_fwd": 1, "qkv_fwd": 1, "attn_fwd": 1, "oproj_fwd": 1, "ln2_fwd": 1, "mlp_up_fwd": 1,
-              "mlp_down_fwd": 1, "mlp_down_bwd_data": 1, "mlp_down_bwd_weight": 1, "mlp_up_bwd_data": 1,
-              "mlp_up_bwd_weight": 1, "ln2_bwd": 2, "oproj_bwd_data": 1, "oproj_bwd_weight": 1, "attn_bwd": 2,
-              "qkv_bwd_data": 1, "qkv_bwd_weight": 1, "ln1_bwd": 2}
-LIB_KERNELS = ("gemm_kernel", "gemm_lds_kernel", "attn_fwd_kernel", "attn_bwd_dq_kernel", "attn_bwd_dkdv_kernel",
-               "ln_fwd_kernel", "ln_bwd_kernel", "ln_bwd_reduce_kernel")
+# GPU kernels of each chain entry, in launch order (a substring of each
+# dispatch's kernel name; every library kernel lives in namespace optimus)
+_GEMM = ("gemm_",)
+_LN_BWD = ("ln_bwd_dx_kernel", "ln_bwd_param_kernel", "ln_bwd_reduce_kernel")
+ENTRY_KERNELS = {"ln1_fwd": ("ln_fwd_kernel",), "qkv_fwd": _GEMM, "attn_fwd": ("attn_fwd_kernel",),
+                 "oproj_fwd": _GEMM, "ln2_fwd": ("ln_fwd_kernel",), "mlp_up_fwd": _GEMM, "mlp_down_fwd": _GEMM,
+                 "mlp_down_bwd_data": _GEMM, "mlp_down_bwd_weight": _GEMM, "mlp_up_bwd_data": _GEMM,
+                 "mlp_up_bwd_weight": _GEMM, "ln2_bwd": _LN_BWD, "oproj_bwd_data": _GEMM,
+                 "oproj_bwd_weight": _GEMM, "attn_bwd": ("attn_bwd_dq_kernel", "attn_bwd_dkdv_kernel"),
+                 "qkv_bwd_data": _GEMM, "qkv_bwd_weight": _GEMM, "ln1_bwd": _LN_BWD}
+DISPATCHES = {n: len(k) for n, k in ENTRY_KERNELS.items()}
+
+
+def is_lib_kernel(name):
+    """A kernel of the layer chain (the measurement reference kernels excluded)."""
+    return "optimus::" in name and "calib_" not in name
+
+
+def map_dispatches(lib):
+    """Split library dispatches [(dispatch id, kernel name, value)] into chain
+    steps and return per step a dict entry -> summed value; every dispatch's
+    name is checked against the entry it is attributed to."""
+    lib = sorted(lib)
+    per_step = sum(DISPATCHES.values())
+    if not lib or len(lib) % per_step:
+        raise RuntimeError(f"{len(lib)} library dispatches is not a whole number of {per_step}-dispatch steps")
+    steps = []
+    for st in range(len(lib) // per_step):
+        i, step = st * per_step, {}
+        for n, kernels in ENTRY_KERNELS.items():
+            for j, k in enumerate(kernels):
+                if k not in lib[i + j][1]:
+                    raise RuntimeError(f"step {st}: dispatch {lib[i + j][0]} ({lib[i + j][1][:80]}) is not {n}/{k}")
+            step[n] = sum(v for _, _, v in lib[i:i + len(kernels)])
+            i += len(kernels)
+        steps.append(step)
+    return steps
+
+
 TRAFFIC_MD = os.path.join(ROOT, "profiles", "vit22b_layer_hbm_traffic.md")
 
 
-def source_hash():
-    """sha256 over the HIP sources: traffic counters describe these kernels only."""
+# Sources each chain entry's kernels are built from (device code and the
+# argument structs they receive): traffic counters describe these files only.
+_COMMON_SRC = ("common.hpp", "lds_dma.hpp", "kernels.hpp")
+_FAMILY_SRC = {"gemm": ("gemm.hip",), "attention": ("attention.hip",), "layernorm": ("layernorm.hip",)}
+
+
+def entry_family(entry):
+    if entry.startswith("ln"):
+        return "layernorm"
+    if entry.startswith("attn"):
+        return "attention"
+    return "gemm"
+
+
+def source_hash(family):
+    """sha256 over the sources of one kernel family."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2408_03505_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted(_FAMILY_SRC[family] + _COMMON_SRC):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
-def _counter_rows(d):
+def _latest_rows(d, pattern):
+    """Rows of the newest rocprofv3 csv matching pattern under d (an output
+    folder may still hold the files of earlier runs)."""
     import csv
     import glob
-    rows = []
-    for f in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)):
-        with open(f) as fh:
-            rows += list(csv.DictReader(fh))
-    return rows
+    files = glob.glob(os.path.join(d, "**", pattern), recursive=True)
+    if not files:
+        return []
+    with open(max(files, key=os.path.getmtime)) as fh:
+        return list(csv.DictReader(fh))
+
+
+def _counter_rows(d):
+    return _latest_rows(d, "*counter_collection.csv")
 
 
 def pmc_traffic(fetch_dir, write_dir, copy_bytes):
@@ -89,18 +143,9 @@ def pmc_traffic(fetch_dir, write_dir, copy_bytes):
         rows = [r for r in _counter_rows(d) if r["Counter_Name"] == ctr]
         copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
         scale = copy_bytes / (max(copies) * 1024.0)
-        lib = sorted(((int(r["Dispatch_Id"]), float(r["Counter_Value"])) for r in rows
-                      if any(k in r["Kernel_Name"] for k in LIB_KERNELS)), key=lambda t: t[0])
-        per_step = sum(DISPATCHES.values())
-        if len(lib) % per_step:
-            raise RuntimeError(f"{len(lib)} library dispatches is not a whole number of steps")
-        steps = len(lib) // per_step
-        out = {n: 0.0 for n in DISPATCHES}
-        for st in range(steps):
-            i = st * per_step
-            for n, k in DISPATCHES.items():
-                out[n] += sum(v for _, v in lib[i:i + k]) * 1024.0 * scale / steps
-                i += k
+        steps = map_dispatches([(int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
+                                for r in rows if is_lib_kernel(r["Kernel_Name"])])
+        out = {n: sum(st[n] for st in steps) * 1024.0 * scale / len(steps) for n in DISPATCHES}
         vals[ctr] = (out, scale)
     return vals
 
@@ -111,7 +156,8 @@ def read_traffic(entry):
     if not os.path.exists(TRAFFIC_MD):
         return None
     text = open(TRAFFIC_MD).read()
-    if f"source-sha256: {source_hash()}" not in text:
+    fam = entry_family(entry)
+    if f"source-sha256 {fam}: {source_hash(fam)}" not in text:
         return None
     for line in text.splitlines():
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
@@ -128,16 +174,10 @@ def summarize(d, skip_steps=0):
     for a kernel trace of this bench also the average duration of each chain
     entry (dispatches mapped by launch order, the first skip_steps steps,
     i.e. the warm-up, left out)."""
-    import csv
-    import glob
     import re
 
     def rows(pattern):
-        out = []
-        for f in sorted(glob.glob(os.path.join(d, "**", pattern), recursive=True)):
-            with open(f) as fh:
-                out += list(csv.DictReader(fh))
-        return out
+        return _latest_rows(d, pattern)
 
     def short(name):
         name = re.sub(r"\(anonymous namespace\)::", "", name)
@@ -145,21 +185,15 @@ def summarize(d, skip_steps=0):
         return name.replace("optimus::", "").replace("void ", "")
 
     trace = rows("*kernel_trace.csv")
-    lib = sorted(((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
-                  for r in trace if any(k in r["Kernel_Name"] for k in LIB_KERNELS)))
-    per_step = sum(DISPATCHES.values())
-    if lib and len(lib) % per_step == 0:
-        steps = len(lib) // per_step
-        acc = {n: [] for n in DISPATCHES}
-        for st in range(skip_steps, steps):
-            i = st * per_step
-            for n, k in DISPATCHES.items():
-                acc[n].append(sum(v for _, v in lib[i:i + k]))
-                i += k
-        print(f"per chain entry, steps {skip_steps}..{steps - 1} (device time of its dispatches):\n")
+    lib = [(int(r["Dispatch_Id"]), r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+           for r in trace if is_lib_kernel(r["Kernel_Name"])]
+    if lib:
+        steps = map_dispatches(lib)[skip_steps:]
+        print(f"per chain entry, steps {skip_steps}..{skip_steps + len(steps) - 1} (device time of its dispatches):\n")
         print("| entry | dispatches | avg us | min us | max us |")
         print("|---|---|---|---|---|")
-        for n, v in acc.items():
+        for n in DISPATCHES:
+            v = [st[n] for st in steps]
             print(f"| {n} | {DISPATCHES[n]} | {np.mean(v):.2f} | {min(v):.2f} | {max(v):.2f} |")
         print()
     groups = {}
@@ -181,6 +215,40 @@ def summarize(d, skip_steps=0):
         print("|---|---|---|---|---|")
         for (k, g, c), v in sorted(agg.items()):
             print(f"| {k} | {g} | {c} | {len(v)} | {np.mean(v):.1f} |")
+
+
+def measure_ceilings(dev, reps=3):
+    """Sustained rates of the library's two reference kernels on this GPU: an
+    MFMA-only bf16 loop (changing operands) and a 1 GiB device copy."""
+    from paper_2408_03505_amd import binding as B
+
+    def best_ms(fn):
+        fn()
+        times = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        return min(times)
+
+    blocks, iters = 1024, 2000
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    ms = best_ms(lambda: B.enc_calib_mfma(blocks, iters, out))
+    mfma = B.calib_mfma_flops(blocks, iters) / (ms * 1e-3) / 1e12
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    ms = best_ms(lambda: B.enc_calib_copy(src, dst))
+    copy = 2 * n / (ms * 1e-3) / 1e9
+    del src, dst
+    props = torch.cuda.get_device_properties(dev)
+    return {"mfma_bf16_tflops": round(mfma, 1), "copy_gbs": round(copy, 1),
+            "compute_units": props.multi_processor_count,
+            "note": "best of 3; MFMA-only loop of v_mfma_f32_32x32x16_bf16 with changing operands; "
+                    "copy counts bytes read plus bytes written"}
 
 
 class Chain:
@@ -302,7 +370,8 @@ def main():
         vals = pmc_traffic(args.pmc_traffic[0], args.pmc_traffic[1], args.copy_mib << 20)
         work = kernel_work(CONFIGS[args.config])
         (fetch, fs), (write, ws) = vals["FETCH_SIZE"], vals["WRITE_SIZE"]
-        print(f"source-sha256: {source_hash()}")
+        for fam in sorted(_FAMILY_SRC):
+            print(f"source-sha256 {fam}: {source_hash(fam)}")
         print(f"copy-reference-bytes: {args.copy_mib << 20}  fetch-scale: {fs:.4f}  write-scale: {ws:.4f}\n")
         print("| entry | FETCH bytes | WRITE bytes | traffic bytes | algorithmic bytes | traffic / algorithmic |")
         print("|---|---|---|---|---|---|")
@@ -379,6 +448,11 @@ def main():
                      "traffic": read_traffic(dom) if args.config == "vit22b" else None,
                      "avg_launch_us": round(avg[dom], 2)},
     }
+    if not args.no_ceilings:
+        ceil = measure_ceilings(dev)
+        res["ceilings"] = ceil
+        res["roofline"]["measured_peak"] = ceil["mfma_bf16_tflops"]
+        res["roofline"]["frac_of_measured"] = round(achieved / ceil["mfma_bf16_tflops"], 4)
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)

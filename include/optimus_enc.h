@@ -257,6 +257,26 @@ int enc_attn_bwd(int batch, int seq, int heads, int head_dim,
                  const enc_bf16 *do_, enc_bf16 *dqkv, void *ws,
                  size_t ws_bytes, enc_stream_t stream);
 
+/* ---- Measurement helpers (not steps of the layer)
+ *
+ * Two reference kernels that bound what the layer's kernels can reach on the
+ * GPU at hand: an MFMA-only loop (the sustained bf16 matrix-core rate under
+ * the clock the chip holds while every matrix core is busy) and a device
+ * copy (the sustained HBM rate).  The caller times them with events on
+ * `stream`; both follow the conventions above. */
+
+/* blocks x 256 threads; every wave issues iters x 16 independent
+ * v_mfma_f32_32x32x16_bf16 on register operands whose mantissa bits change
+ * every iteration, i.e. blocks * 4 * iters * 16 * 32768 flops.  One float
+ * per thread is written to out[blocks * 256] so that nothing is elided.
+ * blocks, iters > 0. */
+int enc_calib_mfma(int blocks, int iters, float *out, enc_stream_t stream);
+
+/* dst[0, bytes) = src[0, bytes) with 16-byte loads and stores.  bytes is a
+ * positive multiple of 16; src and dst are 16-byte aligned and do not
+ * overlap. */
+int enc_calib_copy(const void *src, void *dst, size_t bytes, enc_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

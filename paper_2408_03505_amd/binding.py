@@ -77,6 +77,8 @@ _SIGS = {
     "enc_qkv_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
     "enc_ln_bwd": [_i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_attn_bwd": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_calib_mfma": [_i, _i, _p, _p],
+    "enc_calib_copy": [_p, _p, _sz, _p],
 }
 
 _lib = None
@@ -447,3 +449,31 @@ def enc_attn_bwd(batch, seq, heads, head_dim, qkv, o, lse, do, dqkv=None, ws=Non
     _call("enc_attn_bwd", batch, seq, heads, head_dim, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
           _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
     return dqkv
+
+
+# ---------------------------------------------------------------- measurement helpers
+
+def enc_calib_mfma(blocks, iters, out=None, stream=None, device="cuda"):
+    """MFMA-only reference loop: blocks * 4 * iters * 16 * 32768 flops."""
+    if out is None:
+        out = torch.empty(blocks * 256, dtype=torch.float32, device=device)
+    _check(out, "out", (blocks * 256,), torch.float32)
+    _call("enc_calib_mfma", blocks, iters, _ptr(out), _stream(stream))
+    return out
+
+
+def calib_mfma_flops(blocks, iters):
+    return blocks * 4 * iters * 16 * 32768
+
+
+def enc_calib_copy(src, dst, stream=None):
+    """Reference device copy of src's bytes into dst (both contiguous, same byte size)."""
+    if not (isinstance(src, torch.Tensor) and isinstance(dst, torch.Tensor)):
+        raise TypeError("src and dst must be torch.Tensors")
+    nbytes = src.numel() * src.element_size()
+    if not (src.is_cuda and dst.is_cuda and src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("src and dst must be contiguous device tensors")
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must have the same byte size")
+    _call("enc_calib_copy", _ptr(src), _ptr(dst), nbytes, _stream(stream))
+    return dst

@@ -556,4 +556,30 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   return launched(fn);
 }
 
+// ------------------------------------------------------------ measurement helpers
+
+int enc_calib_mfma(int blocks, int iters, float *out, enc_stream_t stream) {
+  const char *fn = "enc_calib_mfma";
+  int r = check_dims(fn, {blocks, iters});
+  if (r) return r;
+  if (blocks > (1 << 20)) return fail(ENC_ERR_UNSUPPORTED, "%s: at most 2^20 blocks", fn);
+  PtrCheck c(fn);
+  c.req(out, "out");
+  if (c.code) return c.code;
+  launch_calib_mfma(blocks, iters, out, as_stream(stream));
+  return launched(fn);
+}
+
+int enc_calib_copy(const void *src, void *dst, size_t bytes, enc_stream_t stream) {
+  const char *fn = "enc_calib_copy";
+  if (bytes == 0 || bytes % 16) return fail(ENC_ERR_INVALID, "%s: bytes must be a positive multiple of 16", fn);
+  PtrCheck c(fn);
+  c.req(src, "src").req(dst, "dst");
+  if (c.code) return c.code;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(ENC_ERR_INVALID, "%s: src and dst overlap", fn);
+  launch_calib_copy(src, dst, bytes, as_stream(stream));
+  return launched(fn);
+}
+
 }  // extern "C"

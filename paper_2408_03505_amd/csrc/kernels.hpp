@@ -58,4 +58,8 @@ size_t attn_bwd_ws_bytes(int B, int S, int heads);
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s);
 
+// ---- Measurement reference kernels
+bool launch_calib_mfma(int blocks, int iters, float *out, hipStream_t s);
+bool launch_calib_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
+
 }  // namespace optimus

@@ -341,3 +341,17 @@ def test_attn_sequences_are_independent(S, d):
     ref = oracle.attention_bwd(f64(qkv[:S]), f64(dO[:S]), 1, S, nh, d)
     assert np.isfinite(f64(dqkv[:S])).all()
     assert max_rel(f64(dqkv[:S]), ref) < TOL_GRAD
+
+
+# --------------------------------------------------------------------------- measurement helpers
+
+def test_calibration_kernels():
+    announce("calibration kernels")
+    src = torch.randint(0, 256, (1 << 20,), dtype=torch.uint8, device="cuda")
+    dst, buf = guarded((1 << 19,), torch.bfloat16)  # same byte size, guarded tail
+    B.enc_calib_copy(src, dst.view(torch.uint8))
+    out = B.enc_calib_mfma(8, 3)
+    torch.cuda.synchronize()
+    assert torch.equal(dst.view(torch.uint8), src)
+    assert guard_intact(buf, dst.numel())
+    assert torch.isfinite(out).all() and (out > 0).all()

@@ -130,6 +130,20 @@ def test_bad_shapes_are_rejected():
 
 
 @no_gpu_only
+def test_calibration_arguments_are_checked():
+    p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
+    assert _status("enc_calib_mfma", 0, 10, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_calib_mfma", 4, -1, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_calib_mfma", 4, 10, ctypes.c_void_p(0), s) == B.ENC_ERR_INVALID
+    q = ctypes.c_void_p(FAKE + (1 << 20))
+    assert _status("enc_calib_copy", p, q, 0, s) == B.ENC_ERR_INVALID
+    assert _status("enc_calib_copy", p, q, 24, s) == B.ENC_ERR_INVALID
+    assert _status("enc_calib_copy", ctypes.c_void_p(FAKE + 8), q, 32, s) == B.ENC_ERR_ALIGN
+    assert _status("enc_calib_copy", p, ctypes.c_void_p(FAKE + 16), 64, s) == B.ENC_ERR_INVALID  # overlap
+    assert b"overlap" in B.lib().enc_last_error()
+
+
+@no_gpu_only
 def test_small_workspace_is_rejected():
     p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
     need = B.ln_bwd_workspace_bytes(16, 64)
