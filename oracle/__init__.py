@@ -4,4 +4,7 @@ Only the tests, the smoke check and the CPU-baseline leg of the benchmark
 import this package.  The product library never does.
 """
 from .encoder_layer import *  # noqa: F401,F403
-from .encoder_layer import __all__  # noqa: F401
+from .encoder_layer import __all__ as _layer_all
+from . import schedule  # noqa: F401
+
+__all__ = list(_layer_all) + ["schedule"]
