@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--fit-config", default="vit22b_tp8",
+                    help="a second workload whose chain is timed briefly and packed into the synthetic "
+                         "TP-bubble trace beside the main one ('' to skip)")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-only and device-copy reference kernels")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -251,6 +254,65 @@ def measure_ceilings(dev, reps=3):
                     "copy counts bytes read plus bytes written"}
 
 
+FWD_ENTRIES = ("ln1_fwd", "qkv_fwd", "attn_fwd", "oproj_fwd", "ln2_fwd", "mlp_up_fwd", "mlp_down_fwd")
+
+
+def synthetic_tp_trace(seed=0, n=400):
+    """LLM timeline of alternating computation and tensor-parallel bubbles:
+    bubbles uniform in [200, 400] us (about 300 us on average, the TP bubble
+    length the paper profiles), computation uniform in [300, 900] us."""
+    rng = np.random.default_rng(seed)
+    lengths, bubble = [], []
+    for _ in range(n):
+        lengths += [float(rng.uniform(300, 900)), float(rng.uniform(200, 400))]
+        bubble += [False, True]
+    return lengths, bubble
+
+
+def bubble_fit(p50, seed=0):
+    """Pack the chain's forward and backward kernels (per-kernel p50, chain
+    order) into the synthetic TP-bubble trace with the library's packer."""
+    from paper_2408_03505_amd import binding as B
+    lengths, bubble = synthetic_tp_trace(seed)
+    starts = np.concatenate([[0.0], np.cumsum(lengths)[:-1]])
+    out = {}
+    for part, names in (("fwd", [n for n in p50 if n in FWD_ENTRIES]),
+                        ("bwd", [n for n in p50 if n not in FWD_ENTRIES])):
+        kus = [p50[n] for n in names]
+        where, off, placed = B.enc_schedule_kernels(kus, lengths, bubble)
+        r = {"kernels": len(names), "placed": placed, "kernel_us": round(sum(kus), 1)}
+        if placed:
+            used = sorted(set(where[:placed]))
+            r["bubbles_used"] = len(used)
+            r["fill"] = round(sum(kus[:placed]) / sum(lengths[j] for j in used), 3)
+            last = placed - 1
+            r["span_us"] = round(float(starts[where[last]] + off[last] + kus[last] - starts[where[0]]), 1)
+        if placed < len(names):
+            r["blocked_at"] = names[placed]
+            r["blocked_kernel_us"] = round(kus[placed], 1)
+        out[part] = r
+    return out
+
+
+def time_chain(chain, steps, warmup):
+    """Per-entry p50 (us) of a chain, events around every launch."""
+    names = [n for n, _ in chain.kernels]
+    for _ in range(warmup):
+        for _, fn in chain.kernels:
+            fn()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in names]
+          for _ in range(steps)]
+    for k in range(steps):
+        for i, (_, fn) in enumerate(chain.kernels):
+            ev[k][i][0].record()
+            fn()
+            ev[k][i][1].record()
+    torch.cuda.synchronize()
+    return {n: float(np.median([ev[k][i][0].elapsed_time(ev[k][i][1]) * 1e3 for k in range(steps)]))
+            for i, n in enumerate(names)}
+
+
 class Chain:
     """Preallocated buffers and the kernel-by-kernel layer step."""
 
@@ -448,6 +510,18 @@ def main():
                      "traffic": read_traffic(dom) if args.config == "vit22b" else None,
                      "avg_launch_us": round(avg[dom], 2)},
     }
+    fit = {"trace": "synthetic LLM timeline: TP bubbles uniform in [200, 400] us alternating with "
+                    "LLM computation uniform in [300, 900] us (seed 0); kernels = per-kernel p50",
+           args.config: bubble_fit(p50)}
+    if args.fit_config and args.fit_config != args.config:
+        fcfg = CONFIGS[args.fit_config]
+        fx, fp, fd = layer_inputs(fcfg, seed=args.seed)
+        fchain = Chain(fcfg, fx.to(dev), {n: fp[n].to(dev) for n in fp}, fd.to(dev))
+        fp50 = time_chain(fchain, steps=10, warmup=3)
+        fit[args.fit_config] = bubble_fit(fp50)
+        fit[args.fit_config]["p50_us"] = {n: round(v, 2) for n, v in fp50.items()}
+        del fchain
+    res["bubble_fit"] = fit
     if not args.no_ceilings:
         ceil = measure_ceilings(dev)
         res["ceilings"] = ceil

@@ -257,6 +257,33 @@ int enc_attn_bwd(int batch, int seq, int heads, int head_dim,
                  const enc_bf16 *do_, enc_bf16 *dqkv, void *ws,
                  size_t ws_bytes, enc_stream_t stream);
 
+/* ---- Kernel-to-bubble packing (host code, no GPU)
+ *
+ * The bubble scheduler's ScheduleKernels step (§4.2, fine-grained bubble
+ * exploitation): one micro-batch's encoder kernels are placed, in chain
+ * order (the encoder's internal data dependencies), into the LLM timeline.
+ * Computation kernels go into bubbles, several per bubble as long as their
+ * summed time fits; communication kernels are not put into bubbles but
+ * overlapped with LLM computation (§3.1, design decision 3).  Kernels are
+ * never split or reordered: each goes into the earliest interval of its
+ * kind, at or after its predecessor's interval, whose remaining time holds
+ * it -- the componentwise-earliest of all feasible order-keeping placements.
+ *
+ * kernel_us[n_kernels]      durations in chain order (finite, >= 0)
+ * kernel_comm[n_kernels]    1 for a communication kernel; NULL: none is
+ * interval_us[n_intervals]  interval lengths in time order (finite, >= 0)
+ * interval_bubble[n_int.]   1 for a bubble, 0 for a period of LLM computation
+ * out_interval[n_kernels]   interval of each kernel; -1 when it does not fit
+ *                           (every later kernel is then -1 too)
+ * out_offset_us[n_kernels]  start within its interval (-1 if unplaced); may
+ *                           be NULL
+ * All arrays are host memory owned by the caller.  Returns the number of
+ * kernels placed (n_kernels when all fit) or a negative enc_status; outputs
+ * are written only after the arguments validate. */
+int enc_schedule_kernels(const double *kernel_us, const int *kernel_comm, int n_kernels,
+                         const double *interval_us, const int *interval_bubble, int n_intervals,
+                         int *out_interval, double *out_offset_us);
+
 /* ---- Measurement helpers (not steps of the layer)
  *
  * Two reference kernels that bound what the layer's kernels can reach on the

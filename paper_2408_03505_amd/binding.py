@@ -78,6 +78,7 @@ _SIGS = {
     "enc_ln_bwd": [_i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_attn_bwd": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
     "enc_calib_mfma": [_i, _i, _p, _p],
+    "enc_schedule_kernels": [_p, _p, _i, _p, _p, _i, _p, _p],
     "enc_calib_copy": [_p, _p, _sz, _p],
 }
 
@@ -477,3 +478,32 @@ def enc_calib_copy(src, dst, stream=None):
         raise ValueError("src and dst must have the same byte size")
     _call("enc_calib_copy", _ptr(src), _ptr(dst), nbytes, _stream(stream))
     return dst
+
+
+# ---------------------------------------------------------------- kernel-to-bubble packing
+
+def enc_schedule_kernels(kernel_us, interval_us, interval_bubble, kernel_comm=None):
+    """Place kernels (chain order) into timeline intervals; host-side, no GPU.
+
+    Returns (interval index per kernel, -1 if unplaced; start offset in us,
+    -1.0 if unplaced; number placed)."""
+    kus = (ctypes.c_double * len(kernel_us))(*[float(v) for v in kernel_us])
+    ius = (ctypes.c_double * len(interval_us))(*[float(v) for v in interval_us])
+    bub = (ctypes.c_int * len(interval_bubble))(*[1 if b else 0 for b in interval_bubble])
+    if len(interval_bubble) != len(interval_us):
+        raise ValueError("interval_us and interval_bubble differ in length")
+    comm = None
+    if kernel_comm is not None:
+        if len(kernel_comm) != len(kernel_us):
+            raise ValueError("kernel_us and kernel_comm differ in length")
+        comm = (ctypes.c_int * len(kernel_comm))(*[1 if c else 0 for c in kernel_comm])
+    where = (ctypes.c_int * max(1, len(kernel_us)))()
+    off = (ctypes.c_double * max(1, len(kernel_us)))()
+    L = lib()
+    placed = L.enc_schedule_kernels(ctypes.cast(kus, _p), ctypes.cast(comm, _p) if comm is not None else None,
+                                    len(kernel_us), ctypes.cast(ius, _p), ctypes.cast(bub, _p), len(interval_us),
+                                    ctypes.cast(where, _p), ctypes.cast(off, _p))
+    if placed < 0:
+        raise EncError("enc_schedule_kernels", placed, L.enc_last_error().decode())
+    n = len(kernel_us)
+    return list(where)[:n], list(off)[:n], placed

@@ -2,8 +2,9 @@
 
     python -m paper_2408_03505_amd.build
 
-Every .hip file under csrc/ is compiled to an object with hipcc (in
-parallel) and linked into paper_2408_03505_amd/liboptimus_enc.so.  It always
+Every .hip file under csrc/ is compiled to an object with hipcc and every
+.cpp file (host-only code) with the host C++ compiler, in parallel, and all
+are linked into paper_2408_03505_amd/liboptimus_enc.so.  It always
 recompiles: the build is the "does it compile" check as well as the product.
 """
 
@@ -21,6 +22,8 @@ LIB = os.path.join(PKG, "liboptimus_enc.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
+CXX = os.environ.get("CXX", shutil.which("g++") or "c++")
+CXXFLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", f"-I{os.path.join(ROOT, 'include')}"]
 CFLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
@@ -34,16 +37,19 @@ CFLAGS = [
 
 def _compile(src):
     obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    if src.endswith(".cpp"):
+        cmd = [CXX, *CXXFLAGS, "-c", src, "-o", obj]
+    else:
+        cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+        raise RuntimeError(f"compiling {src} failed:\n{r.stdout}\n{r.stderr}")
     return obj
 
 
 def build(verbose=True):
     os.makedirs(OBJ, exist_ok=True)
-    srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     tmp = LIB + ".tmp"

@@ -7,14 +7,15 @@
 
 #include "../../include/optimus_enc.h"
 #include "kernels.hpp"
+#include "status.hpp"
 
 using namespace optimus;
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
 
-int fail(int code, const char *fmt, ...) {
+int optimus::set_error(int code, const char *fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -24,10 +25,19 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
-int ok() {
+int optimus::clear_error() {
   g_last_error.clear();
   return ENC_OK;
 }
+
+namespace {
+
+template <typename... Args>
+int fail(int code, const char *fmt, Args... args) {
+  return set_error(code, fmt, args...);
+}
+
+int ok() { return clear_error(); }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
