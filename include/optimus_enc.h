@@ -157,7 +157,8 @@ int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma,
                const enc_bf16 *beta, float eps, enc_bf16 *y, float *mean,
                float *rstd, enc_stream_t stream);
 
-/* QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A]. */
+/* QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A].
+ * b_qkv may be NULL (no bias, as in the ViT-22B-style block below). */
 int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv,
                 const enc_bf16 *b_qkv, enc_bf16 *qkv, enc_stream_t stream);
 
@@ -256,6 +257,98 @@ int enc_attn_bwd(int batch, int seq, int heads, int head_dim,
                  const enc_bf16 *qkv, const enc_bf16 *o, const float *lse,
                  const enc_bf16 *do_, enc_bf16 *dqkv, void *ws,
                  size_t ws_bytes, enc_stream_t stream);
+
+/* ------------------------------------------------------------ ViT-22B-style block
+ *
+ * The paper's largest encoder is ViT-22B (Appendix A).  The cited ViT-22B
+ * architecture differs from the sequential pre-LN block above: attention and
+ * MLP run in parallel on one LayerNorm of the input, queries and keys are
+ * layer-normalised per head before the dot product, and the QKV projection
+ * has no bias:
+ *   y    = LN(x)                          (ln_g, ln_b over H)
+ *   qkv  = y * w_qkv^T                    (no bias)
+ *   qkvn = QKnorm(qkv)                    (LN over head_dim of every query and
+ *                                          key vector: qn_g, qn_b, kn_g, kn_b
+ *                                          of length head_dim, shared by heads;
+ *                                          values unchanged)
+ *   o    = Attn(qkvn)                     (as enc_attn_fwd)
+ *   h    = x + o * w_o^T + b_o            (residual + attention branch)
+ *   out  = h + GELU(y * w_1^T + b_1) * w_2^T + b_2   (+ MLP branch, fed by y)
+ * Every LayerNorm uses cfg->ln_eps.  Shapes as in enc_params_t, plus the four
+ * QK-norm vectors of length head_dim. */
+typedef struct {
+  const enc_bf16 *ln_g, *ln_b;               /* [H] */
+  const enc_bf16 *w_qkv;                     /* [3A, H] */
+  const enc_bf16 *qn_g, *qn_b, *kn_g, *kn_b; /* [head_dim] */
+  const enc_bf16 *w_o, *b_o;                 /* [H, A], [H] */
+  const enc_bf16 *w_1, *b_1;                 /* [F, H], [F] */
+  const enc_bf16 *w_2, *b_2;                 /* [H, F], [H] */
+} enc_pparams_t;
+
+/* fp32 parameter gradients, same shapes as enc_pparams_t. */
+typedef struct {
+  float *ln_g, *ln_b, *w_qkv, *qn_g, *qn_b, *kn_g, *kn_b, *w_o, *b_o, *w_1, *b_1, *w_2, *b_2;
+} enc_pgrads_t;
+
+/* Byte offsets (multiples of 256) of the block's saved tensors in one caller
+ * buffer.  bf16: y, h [M,H]; qkv, qkvn [M,3A]; o [M,A]; u, g [M,F].  fp32:
+ * mean, rstd [M]; qkstats [M, heads, 4] = (query mean, query rstd, key mean,
+ * key rstd) per token and head; lse [batch, heads, seq]. */
+typedef struct {
+  size_t y, mean, rstd, qkv, qkvn, qkstats, o, lse, h, u, g;
+  size_t total;
+} enc_psaved_layout_t;
+
+int enc_parallel_saved_layout(const enc_cfg_t *cfg, enc_psaved_layout_t *layout);
+/* Workspace bytes encoder_parallel_bwd needs. */
+int enc_parallel_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes);
+
+/* Forward of the block: LN, QKV projection, QK norm, attention, output
+ * projection + residual, MLP up + GELU (from y), MLP down + residual, on one
+ * stream.  x, out: [M, H]; saved: enc_parallel_saved_layout().total bytes. */
+int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params,
+                         const enc_bf16 *x, enc_bf16 *out, void *saved,
+                         enc_stream_t stream);
+
+/* Exact gradient of encoder_parallel_fwd.  dy of the shared LayerNorm is the
+ * sum of both branches' input gradients (the QKV input gradient adds the
+ * MLP branch's in its epilogue); dx = dout + LN backward(dy).  accumulate as
+ * for encoder_layer_bwd; deterministic. */
+int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params,
+                         const enc_bf16 *x, const void *saved,
+                         const enc_bf16 *dout, enc_bf16 *dx,
+                         const enc_pgrads_t *grads, int accumulate, void *ws,
+                         size_t ws_bytes, enc_stream_t stream);
+
+/* QK normalisation: qkvn = qkv with every (token, head) query vector replaced
+ * by LN(q) * qn_g + qn_b and every key vector by LN(k) * kn_g + kn_b (LN over
+ * head_dim, biased variance, eps inside the square root); values copied.
+ * qkv, qkvn: [M, 3*heads*head_dim]; stats: [M, heads, 4] fp32 (query mean,
+ * query rstd, key mean, key rstd).  head_dim in {64, 80, 128}. */
+int enc_qk_norm_fwd(int M, int heads, int head_dim, const enc_bf16 *qkv,
+                    const enc_bf16 *qn_g, const enc_bf16 *qn_b,
+                    const enc_bf16 *kn_g, const enc_bf16 *kn_b, float eps,
+                    enc_bf16 *qkvn, float *stats, enc_stream_t stream);
+
+int enc_qk_norm_bwd_workspace_bytes(int M, int heads, int head_dim, size_t *bytes);
+
+/* Gradient of enc_qk_norm_fwd: dqkv from dqkvn (LayerNorm backward for
+ * queries and keys, values copied) and the fp32 gradients of the four
+ * affine vectors, summed over tokens and heads in a fixed order (overwritten,
+ * or added with accumulate=1).  ws: enc_qk_norm_bwd_workspace_bytes. */
+int enc_qk_norm_bwd(int M, int heads, int head_dim, const enc_bf16 *dqkvn,
+                    const enc_bf16 *qkv, const float *stats,
+                    const enc_bf16 *qn_g, const enc_bf16 *kn_g, enc_bf16 *dqkv,
+                    float *dqn_g, float *dqn_b, float *dkn_g, float *dkn_b,
+                    int accumulate, void *ws, size_t ws_bytes,
+                    enc_stream_t stream);
+
+/* QKV input gradient plus an addend (the other branch's input gradient of
+ * the shared LayerNorm output): dy[M, H] = dqkv[M, 3A] * w_qkv[3A, H] +
+ * addend[M, H], accumulated in fp32 before one rounding to bf16. */
+int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv,
+                         const enc_bf16 *w_qkv, const enc_bf16 *addend,
+                         enc_bf16 *dy, enc_stream_t stream);
 
 /* ---- Kernel-to-bubble packing (host code, no GPU)
  *

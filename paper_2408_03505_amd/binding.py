@@ -20,6 +20,8 @@ LIB_PATH = os.path.join(_HERE, "liboptimus_enc.so")
 PARAM_ORDER = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
                "ln2_g", "ln2_b", "w_1", "b_1", "w_2", "b_2")
 SAVED_FIELDS = ("y1", "mean1", "rstd1", "qkv", "o", "lse", "h", "y2", "mean2", "rstd2", "u", "g")
+PPARAM_ORDER = ("ln_g", "ln_b", "w_qkv", "qn_g", "qn_b", "kn_g", "kn_b", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2")
+PSAVED_FIELDS = ("y", "mean", "rstd", "qkv", "qkvn", "qkstats", "o", "lse", "h", "u", "g")
 
 ENC_OK, ENC_ERR_INVALID, ENC_ERR_UNSUPPORTED, ENC_ERR_ALIGN, ENC_ERR_LAUNCH, ENC_ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 
@@ -46,6 +48,18 @@ class EncGrads(ctypes.Structure):
 
 class EncSavedLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in SAVED_FIELDS] + [("total", ctypes.c_size_t)]
+
+
+class EncPParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PPARAM_ORDER]
+
+
+class EncPGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PPARAM_ORDER]
+
+
+class EncPSavedLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in PSAVED_FIELDS] + [("total", ctypes.c_size_t)]
 
 
 _i, _f, _p, _sz = ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
@@ -79,6 +93,15 @@ _SIGS = {
     "enc_attn_bwd": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
     "enc_calib_mfma": [_i, _i, _p, _p],
     "enc_schedule_kernels": [_p, _p, _i, _p, _p, _i, _p, _p],
+    "enc_parallel_saved_layout": [_PCFG, ctypes.POINTER(EncPSavedLayout)],
+    "enc_parallel_workspace_bytes": [_PCFG, ctypes.POINTER(_sz)],
+    "encoder_parallel_fwd": [_PCFG, ctypes.POINTER(EncPParams), _p, _p, _p, _p],
+    "encoder_parallel_bwd": [_PCFG, ctypes.POINTER(EncPParams), _p, _p, _p, _p, ctypes.POINTER(EncPGrads), _i, _p,
+                             _sz, _p],
+    "enc_qk_norm_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _f, _p, _p, _p],
+    "enc_qk_norm_bwd_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
+    "enc_qk_norm_bwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_qkv_bwd_data_add": [_i, _i, _i, _p, _p, _p, _p, _p],
     "enc_calib_copy": [_p, _p, _sz, _p],
 }
 
@@ -264,7 +287,8 @@ def enc_qkv_fwd(y1, w_qkv, b_qkv, qkv=None, stream=None):
     A3 = w_qkv.shape[0]
     _check(y1, "y1", (M, H))
     _check(w_qkv, "w_qkv", (A3, H))
-    _check(b_qkv, "b_qkv", (A3,))
+    if b_qkv is not None:
+        _check(b_qkv, "b_qkv", (A3,))
     qkv = _out(qkv, "qkv", (M, A3), y1)
     if A3 % 3:
         raise ValueError("w_qkv rows must be 3*A")
@@ -507,3 +531,137 @@ def enc_schedule_kernels(kernel_us, interval_us, interval_bubble, kernel_comm=No
         raise EncError("enc_schedule_kernels", placed, L.enc_last_error().decode())
     n = len(kernel_us)
     return list(where)[:n], list(off)[:n], placed
+
+
+# ---------------------------------------------------------------- ViT-22B-style parallel block
+
+def parallel_param_shapes(cfg):
+    H, A, F, d = cfg["hidden"], cfg["heads"] * cfg["head_dim"], cfg["mlp"], cfg["head_dim"]
+    return {"ln_g": (H,), "ln_b": (H,), "w_qkv": (3 * A, H), "qn_g": (d,), "qn_b": (d,), "kn_g": (d,),
+            "kn_b": (d,), "w_o": (H, A), "b_o": (H,), "w_1": (F, H), "b_1": (F,), "w_2": (H, F), "b_2": (H,)}
+
+
+def parallel_saved_layout(cfg):
+    L = EncPSavedLayout()
+    c = make_cfg(cfg)
+    _call("enc_parallel_saved_layout", ctypes.byref(c), ctypes.byref(L))
+    return {n: getattr(L, n) for n in PSAVED_FIELDS + ("total",)}
+
+
+def parallel_workspace_bytes(cfg):
+    n = ctypes.c_size_t()
+    c = make_cfg(cfg)
+    _call("enc_parallel_workspace_bytes", ctypes.byref(c), ctypes.byref(n))
+    return n.value
+
+
+def parallel_saved_views(cfg, saved):
+    """Typed views of the parallel block's saved buffer (uint8 tensor)."""
+    lay = parallel_saved_layout(cfg)
+    M, nh = cfg["batch"] * cfg["seq"], cfg["heads"]
+    H, A, F = cfg["hidden"], nh * cfg["head_dim"], cfg["mlp"]
+    bf, f32 = torch.bfloat16, torch.float32
+    spec = {"y": ((M, H), bf), "mean": ((M,), f32), "rstd": ((M,), f32), "qkv": ((M, 3 * A), bf),
+            "qkvn": ((M, 3 * A), bf), "qkstats": ((M, nh, 4), f32), "o": ((M, A), bf),
+            "lse": ((cfg["batch"], nh, cfg["seq"]), f32), "h": ((M, H), bf), "u": ((M, F), bf), "g": ((M, F), bf)}
+    out = {}
+    for n, (shape, dt) in spec.items():
+        nbytes = int(torch.Size(shape).numel()) * (2 if dt == bf else 4)
+        out[n] = saved[lay[n]:lay[n] + nbytes].view(dt).view(shape)
+    return out
+
+
+def _pparams_struct(cfg, params):
+    shapes = parallel_param_shapes(cfg)
+    return EncPParams(*[_ptr(_check(params[n], n, shapes[n])) for n in PPARAM_ORDER])
+
+
+def encoder_parallel_fwd(cfg, params, x, out=None, saved=None, stream=None):
+    """Forward of the parallel block. Returns (out, saved)."""
+    M, H = cfg["batch"] * cfg["seq"], cfg["hidden"]
+    _check(x, "x", (M, H))
+    out = _out(out, "out", (M, H), x)
+    total = parallel_saved_layout(cfg)["total"]
+    saved = _out(saved, "saved", (total,), x, torch.uint8)
+    c, p = make_cfg(cfg), _pparams_struct(cfg, params)
+    _call("encoder_parallel_fwd", ctypes.byref(c), ctypes.byref(p), _ptr(x), _ptr(out), _ptr(saved), _stream(stream))
+    return out, saved
+
+
+def encoder_parallel_bwd(cfg, params, x, saved, dout, grads=None, dx=None, accumulate=False, ws=None, stream=None):
+    """Backward of the parallel block. Returns (dx, grads) with fp32 grads."""
+    M, H = cfg["batch"] * cfg["seq"], cfg["hidden"]
+    _check(x, "x", (M, H))
+    _check(dout, "dout", (M, H))
+    dx = _out(dx, "dx", (M, H), x)
+    shapes = parallel_param_shapes(cfg)
+    if grads is None:
+        if accumulate:
+            raise ValueError("accumulate=True needs existing grads")
+        grads = {n: torch.empty(shapes[n], dtype=torch.float32, device=x.device) for n in PPARAM_ORDER}
+    for n in PPARAM_ORDER:
+        _check(grads[n], "d" + n, shapes[n], torch.float32)
+    if ws is None:
+        ws = torch.empty(parallel_workspace_bytes(cfg), dtype=torch.uint8, device=x.device)
+    _check(saved, "saved", (parallel_saved_layout(cfg)["total"],), torch.uint8)
+    c, p = make_cfg(cfg), _pparams_struct(cfg, params)
+    g = EncPGrads(*[_ptr(grads[n]) for n in PPARAM_ORDER])
+    _call("encoder_parallel_bwd", ctypes.byref(c), ctypes.byref(p), _ptr(x), _ptr(saved), _ptr(dout), _ptr(dx),
+          ctypes.byref(g), 1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream))
+    return dx, grads
+
+
+def qk_norm_bwd_workspace_bytes(M, heads, head_dim):
+    n = ctypes.c_size_t()
+    _call("enc_qk_norm_bwd_workspace_bytes", M, heads, head_dim, ctypes.byref(n))
+    return n.value
+
+
+def enc_qk_norm_fwd(heads, head_dim, qkv, qn_g, qn_b, kn_g, kn_b, eps, qkvn=None, stats=None, stream=None):
+    M = qkv.shape[0]
+    A = heads * head_dim
+    _check(qkv, "qkv", (M, 3 * A))
+    for n, t in (("qn_g", qn_g), ("qn_b", qn_b), ("kn_g", kn_g), ("kn_b", kn_b)):
+        _check(t, n, (head_dim,))
+    qkvn = _out(qkvn, "qkvn", (M, 3 * A), qkv)
+    stats = _out(stats, "stats", (M, heads, 4), qkv, torch.float32)
+    _call("enc_qk_norm_fwd", M, heads, head_dim, _ptr(qkv), _ptr(qn_g), _ptr(qn_b), _ptr(kn_g), _ptr(kn_b),
+          float(eps), _ptr(qkvn), _ptr(stats), _stream(stream))
+    return qkvn, stats
+
+
+def enc_qk_norm_bwd(heads, head_dim, dqkvn, qkv, stats, qn_g, kn_g, dqkv=None, grads=None, accumulate=False,
+                    ws=None, stream=None):
+    """Returns (dqkv, grads) with grads a dict of fp32 qn_g, qn_b, kn_g, kn_b."""
+    M = qkv.shape[0]
+    A = heads * head_dim
+    _check(dqkvn, "dqkvn", (M, 3 * A))
+    _check(qkv, "qkv", (M, 3 * A))
+    _check(stats, "stats", (M, heads, 4), torch.float32)
+    _check(qn_g, "qn_g", (head_dim,))
+    _check(kn_g, "kn_g", (head_dim,))
+    dqkv = _out(dqkv, "dqkv", (M, 3 * A), qkv)
+    names = ("qn_g", "qn_b", "kn_g", "kn_b")
+    if grads is None:
+        if accumulate:
+            raise ValueError("accumulate=True needs existing grads")
+        grads = {n: torch.empty(head_dim, dtype=torch.float32, device=qkv.device) for n in names}
+    for n in names:
+        _check(grads[n], "d" + n, (head_dim,), torch.float32)
+    if ws is None:
+        ws = torch.empty(qk_norm_bwd_workspace_bytes(M, heads, head_dim), dtype=torch.uint8, device=qkv.device)
+    _call("enc_qk_norm_bwd", M, heads, head_dim, _ptr(dqkvn), _ptr(qkv), _ptr(stats), _ptr(qn_g), _ptr(kn_g),
+          _ptr(dqkv), *[_ptr(grads[n]) for n in names], 1 if accumulate else 0, _ptr(ws), ws.numel(),
+          _stream(stream))
+    return dqkv, grads
+
+
+def enc_qkv_bwd_data_add(dqkv, w_qkv, addend, dy=None, stream=None):
+    M, A3 = dqkv.shape
+    H = w_qkv.shape[1]
+    _check(dqkv, "dqkv", (M, A3))
+    _check(w_qkv, "w_qkv", (A3, H))
+    _check(addend, "addend", (M, H))
+    dy = _out(dy, "dy", (M, H), dqkv)
+    _call("enc_qkv_bwd_data_add", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(addend), _ptr(dy), _stream(stream))
+    return dy

@@ -201,6 +201,16 @@ bool gemm_dgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf
   return launch_gemm_dgrad(a, U ? Epi::kGeluGrad : Epi::kPlain, s);
 }
 
+// dX[M, K] = dY[M, N] * W[N, K] + R[M, K]
+bool gemm_dgrad_add(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *R, bf16_t *dX,
+                    hipStream_t s) {
+  GemmArgs a{};
+  a.M = M, a.N = K, a.K = N;
+  a.A = dY, a.lda = N, a.B = W, a.ldb = K;
+  a.Y = dX, a.ldy = K, a.R = R;
+  return launch_gemm_dgrad(a, Epi::kResid, s);
+}
+
 // dW[N, K] (+)= dY[M, N]^T X[M, K]; db[N] (+)= sum_m dY
 bool gemm_wgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *X, float *dW, float *db, int acc, hipStream_t s) {
   GemmArgs a{};
@@ -229,6 +239,83 @@ int attn_dims(const char *fn, int B, int S, int heads, int d) {
   if (static_cast<long>(B) * S * 3 * heads * d >= kMaxElems)
     return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
   return ENC_OK;
+}
+
+int qk_dims(const char *fn, int M, int heads, int d) {
+  int r = check_dims(fn, {M, heads, d});
+  if (r) return r;
+  if (d != 64 && d != 80 && d != 128) return fail(ENC_ERR_UNSUPPORTED, "%s: head_dim must be 64, 80 or 128", fn);
+  if (static_cast<long>(M) * 3 * heads * d >= kMaxElems)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+void psaved_layout(const enc_cfg_t *c, enc_psaved_layout_t *L) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  const size_t H = c->hidden, A = static_cast<size_t>(c->heads) * c->head_dim, F = c->mlp;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  };
+  L->y = take(M * H * 2);
+  L->mean = take(M * 4);
+  L->rstd = take(M * 4);
+  L->qkv = take(M * 3 * A * 2);
+  L->qkvn = take(M * 3 * A * 2);
+  L->qkstats = take(M * c->heads * 4 * 4);
+  L->o = take(M * A * 2);
+  L->lse = take(static_cast<size_t>(c->batch) * c->heads * c->seq * 4);
+  L->h = take(M * H * 2);
+  L->u = take(M * F * 2);
+  L->g = take(M * F * 2);
+  L->total = off;
+}
+
+struct PBwdWs {
+  size_t du, dy_mlp, dO, dqkvn, dqkv, dy, ln_part, dvec, qk_part, total;
+};
+
+PBwdWs pbwd_layout(const enc_cfg_t *c) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  const size_t H = c->hidden, A = static_cast<size_t>(c->heads) * c->head_dim, F = c->mlp;
+  PBwdWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  };
+  w.du = take(M * F * 2);
+  w.dy_mlp = take(M * H * 2);
+  w.dO = take(M * A * 2);
+  w.dqkvn = take(M * 3 * A * 2);
+  w.dqkv = take(M * 3 * A * 2);
+  w.dy = take(M * H * 2);
+  w.ln_part = take(ln_bwd_ws_bytes(static_cast<int>(M), c->hidden));
+  w.dvec = take(attn_bwd_ws_bytes(c->batch, c->seq, c->heads));
+  w.qk_part = take(qk_norm_bwd_ws_bytes(static_cast<int>(M), c->heads, c->head_dim));
+  w.total = off;
+  return w;
+}
+
+int check_pparams(const char *fn, const enc_pparams_t *p) {
+  if (!p) return fail(ENC_ERR_INVALID, "%s: params is NULL", fn);
+  PtrCheck c(fn);
+  c.req(p->ln_g, "ln_g").req(p->ln_b, "ln_b").req(p->w_qkv, "w_qkv").req(p->qn_g, "qn_g").req(p->qn_b, "qn_b");
+  c.req(p->kn_g, "kn_g").req(p->kn_b, "kn_b").req(p->w_o, "w_o").req(p->b_o, "b_o");
+  c.req(p->w_1, "w_1").req(p->b_1, "b_1").req(p->w_2, "w_2").req(p->b_2, "b_2");
+  return c.code;
+}
+
+int check_pgrads(const char *fn, const enc_pgrads_t *g) {
+  if (!g) return fail(ENC_ERR_INVALID, "%s: grads is NULL", fn);
+  PtrCheck c(fn);
+  c.req(g->ln_g, "dln_g").req(g->ln_b, "dln_b").req(g->w_qkv, "dw_qkv").req(g->qn_g, "dqn_g").req(g->qn_b, "dqn_b");
+  c.req(g->kn_g, "dkn_g").req(g->kn_b, "dkn_b").req(g->w_o, "dw_o").req(g->b_o, "db_o");
+  c.req(g->w_1, "dw_1").req(g->b_1, "db_1").req(g->w_2, "dw_2").req(g->b_2, "db_2");
+  return c.code;
 }
 
 }  // namespace
@@ -307,9 +394,10 @@ int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv, 
   int r = linear_dims(fn, M, {H, A, 3 * A});
   if (r) return r;
   PtrCheck c(fn);
-  c.req(y1, "y1").req(w_qkv, "w_qkv").req(b_qkv, "b_qkv").req(qkv, "qkv");
+  c.req(y1, "y1").req(w_qkv, "w_qkv").opt(b_qkv, "b_qkv").req(qkv, "qkv");
   if (c.code) return c.code;
-  if (!gemm_fwd(M, 3 * A, H, y1, w_qkv, b_qkv, nullptr, qkv, nullptr, Epi::kBias, as_stream(stream)))
+  if (!gemm_fwd(M, 3 * A, H, y1, w_qkv, b_qkv, nullptr, qkv, nullptr, b_qkv ? Epi::kBias : Epi::kPlain,
+                as_stream(stream)))
     return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
   return launched(fn);
 }
@@ -413,6 +501,19 @@ int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *
   c.req(dqkv, "dqkv").req(w_qkv, "w_qkv").req(dy1, "dy1");
   if (c.code) return c.code;
   if (!gemm_dgrad(M, 3 * A, H, dqkv, w_qkv, nullptr, dy1, as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  return launched(fn);
+}
+
+int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *w_qkv, const enc_bf16 *addend,
+                         enc_bf16 *dy, enc_stream_t stream) {
+  const char *fn = "enc_qkv_bwd_data_add";
+  int r = linear_dims(fn, M, {H, A, 3 * A});
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dqkv, "dqkv").req(w_qkv, "w_qkv").req(addend, "addend").req(dy, "dy");
+  if (c.code) return c.code;
+  if (!gemm_dgrad_add(M, 3 * A, H, dqkv, w_qkv, addend, dy, as_stream(stream)))
     return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
   return launched(fn);
 }
@@ -562,6 +663,143 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, s);       // dy1 = dqkv Wqkv
   okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, s);  // dWqkv, dbqkv
   okk = okk && launch_ln_bwd(M, H, dy1, x, mean1, rstd1, p.ln1_g, dh, dx, gr.ln1_g, gr.ln1_b, acc, part, s);
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+// ------------------------------------------------------------ ViT-22B-style parallel block
+
+int enc_qk_norm_fwd(int M, int heads, int head_dim, const enc_bf16 *qkv, const enc_bf16 *qn_g, const enc_bf16 *qn_b,
+                    const enc_bf16 *kn_g, const enc_bf16 *kn_b, float eps, enc_bf16 *qkvn, float *stats,
+                    enc_stream_t stream) {
+  const char *fn = "enc_qk_norm_fwd";
+  int r = qk_dims(fn, M, heads, head_dim);
+  if (r) return r;
+  if (!(eps >= 0.f)) return fail(ENC_ERR_INVALID, "%s: eps must be >= 0", fn);
+  PtrCheck c(fn);
+  c.req(qkv, "qkv").req(qn_g, "qn_g").req(qn_b, "qn_b").req(kn_g, "kn_g").req(kn_b, "kn_b");
+  c.req(qkvn, "qkvn").req(stats, "stats");
+  if (c.code) return c.code;
+  launch_qk_norm_fwd(M, heads, head_dim, qkv, qn_g, qn_b, kn_g, kn_b, eps, qkvn, stats, as_stream(stream));
+  return launched(fn);
+}
+
+int enc_qk_norm_bwd_workspace_bytes(int M, int heads, int head_dim, size_t *bytes) {
+  const char *fn = "enc_qk_norm_bwd_workspace_bytes";
+  int r = qk_dims(fn, M, heads, head_dim);
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = qk_norm_bwd_ws_bytes(M, heads, head_dim);
+  return ok();
+}
+
+int enc_qk_norm_bwd(int M, int heads, int head_dim, const enc_bf16 *dqkvn, const enc_bf16 *qkv, const float *stats,
+                    const enc_bf16 *qn_g, const enc_bf16 *kn_g, enc_bf16 *dqkv, float *dqn_g, float *dqn_b,
+                    float *dkn_g, float *dkn_b, int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "enc_qk_norm_bwd";
+  int r = qk_dims(fn, M, heads, head_dim);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dqkvn, "dqkvn").req(qkv, "qkv").req(stats, "stats").req(qn_g, "qn_g").req(kn_g, "kn_g");
+  c.req(dqkv, "dqkv").req(dqn_g, "dqn_g").req(dqn_b, "dqn_b").req(dkn_g, "dkn_g").req(dkn_b, "dkn_b").req(ws, "ws");
+  if (c.code) return c.code;
+  const size_t need = qk_norm_bwd_ws_bytes(M, heads, head_dim);
+  if (ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  launch_qk_norm_bwd(M, heads, head_dim, dqkvn, qkv, stats, qn_g, kn_g, dqkv, dqn_g, dqn_b, dkn_g, dkn_b,
+                     accumulate ? 1 : 0, static_cast<float *>(ws), as_stream(stream));
+  return launched(fn);
+}
+
+int enc_parallel_saved_layout(const enc_cfg_t *cfg, enc_psaved_layout_t *layout) {
+  const char *fn = "enc_parallel_saved_layout";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (!layout) return fail(ENC_ERR_INVALID, "%s: layout is NULL", fn);
+  psaved_layout(cfg, layout);
+  return ok();
+}
+
+int enc_parallel_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes) {
+  const char *fn = "enc_parallel_workspace_bytes";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = pbwd_layout(cfg).total;
+  return ok();
+}
+
+int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params, const enc_bf16 *x, enc_bf16 *out,
+                         void *saved, enc_stream_t stream) {
+  const char *fn = "encoder_parallel_fwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if ((r = check_pparams(fn, params))) return r;
+  PtrCheck c(fn);
+  c.req(x, "x").req(out, "out").req(saved, "saved");
+  if (c.code) return c.code;
+  enc_psaved_layout_t L;
+  psaved_layout(cfg, &L);
+  const int M = cfg->batch * cfg->seq, H = cfg->hidden, F = cfg->mlp, A = cfg->heads * cfg->head_dim;
+  const hipStream_t s = as_stream(stream);
+  const enc_pparams_t &p = *params;
+  bf16_t *y = at<bf16_t>(saved, L.y), *qkv = at<bf16_t>(saved, L.qkv), *qkvn = at<bf16_t>(saved, L.qkvn);
+  bf16_t *o = at<bf16_t>(saved, L.o), *h = at<bf16_t>(saved, L.h), *u = at<bf16_t>(saved, L.u);
+  bf16_t *g = at<bf16_t>(saved, L.g);
+  float *mean = at<float>(saved, L.mean), *rstd = at<float>(saved, L.rstd), *lse = at<float>(saved, L.lse);
+  float *qks = at<float>(saved, L.qkstats);
+
+  bool okk = launch_ln_fwd(M, H, x, p.ln_g, p.ln_b, cfg->ln_eps, y, mean, rstd, s);
+  okk = okk && gemm_fwd(M, 3 * A, H, y, p.w_qkv, nullptr, nullptr, qkv, nullptr, Epi::kPlain, s);
+  okk = okk && launch_qk_norm_fwd(M, cfg->heads, cfg->head_dim, qkv, p.qn_g, p.qn_b, p.kn_g, p.kn_b, cfg->ln_eps,
+                                  qkvn, qks, s);
+  okk = okk && launch_attn_fwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkvn, o, lse, s);
+  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, s);   // x + attention branch
+  okk = okk && gemm_fwd(M, F, H, y, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);    // MLP reads y too
+  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);  // + MLP branch
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params, const enc_bf16 *x, const void *saved,
+                         const enc_bf16 *dout, enc_bf16 *dx, const enc_pgrads_t *grads, int accumulate, void *ws,
+                         size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "encoder_parallel_bwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if ((r = check_pparams(fn, params))) return r;
+  if ((r = check_pgrads(fn, grads))) return r;
+  PtrCheck c(fn);
+  c.req(x, "x").req(saved, "saved").req(dout, "dout").req(dx, "dx").req(ws, "ws");
+  if (c.code) return c.code;
+  const PBwdWs W = pbwd_layout(cfg);
+  if (ws_bytes < W.total) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, W.total);
+  enc_psaved_layout_t L;
+  psaved_layout(cfg, &L);
+  const int M = cfg->batch * cfg->seq, H = cfg->hidden, F = cfg->mlp, A = cfg->heads * cfg->head_dim;
+  const int acc = accumulate ? 1 : 0;
+  const hipStream_t s = as_stream(stream);
+  const enc_pparams_t &p = *params;
+  const enc_pgrads_t &gr = *grads;
+  const bf16_t *y = at<bf16_t>(saved, L.y), *qkv = at<bf16_t>(saved, L.qkv), *qkvn = at<bf16_t>(saved, L.qkvn);
+  const bf16_t *o = at<bf16_t>(saved, L.o), *u = at<bf16_t>(saved, L.u), *g = at<bf16_t>(saved, L.g);
+  const float *mean = at<float>(saved, L.mean), *rstd = at<float>(saved, L.rstd), *lse = at<float>(saved, L.lse);
+  const float *qks = at<float>(saved, L.qkstats);
+  bf16_t *du = at<bf16_t>(ws, W.du), *dy_mlp = at<bf16_t>(ws, W.dy_mlp), *dO = at<bf16_t>(ws, W.dO);
+  bf16_t *dqkvn = at<bf16_t>(ws, W.dqkvn), *dqkv = at<bf16_t>(ws, W.dqkv), *dy = at<bf16_t>(ws, W.dy);
+  float *ln_part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec), *qk_part = at<float>(ws, W.qk_part);
+
+  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                  // du = dout W2 * GELU'(u)
+  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, s);      // dW2, db2
+  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy_mlp, s);        // MLP branch's dy
+  okk = okk && gemm_wgrad(M, F, H, du, y, gr.w_1, gr.b_1, acc, s);        // dW1, db1
+  okk = okk && gemm_dgrad(M, H, A, dout, p.w_o, nullptr, dO, s);          // dO = dout Wo
+  okk = okk && gemm_wgrad(M, H, A, dout, o, gr.w_o, gr.b_o, acc, s);      // dWo, dbo
+  okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkvn, o, lse, dO, dqkvn, dvec, s);
+  okk = okk && launch_qk_norm_bwd(M, cfg->heads, cfg->head_dim, dqkvn, qkv, qks, p.qn_g, p.kn_g, dqkv, gr.qn_g,
+                                  gr.qn_b, gr.kn_g, gr.kn_b, acc, qk_part, s);
+  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y, gr.w_qkv, nullptr, acc, s);  // dWqkv (no bias)
+  okk = okk && gemm_dgrad_add(M, 3 * A, H, dqkv, p.w_qkv, dy_mlp, dy, s);   // dy = dqkv Wqkv + dy_mlp
+  okk = okk && launch_ln_bwd(M, H, dy, x, mean, rstd, p.ln_g, dout, dx, gr.ln_g, gr.ln_b, acc, ln_part, s);
   if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
   return launched(fn);
 }

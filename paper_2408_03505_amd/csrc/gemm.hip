@@ -90,7 +90,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs &p, const f32x16_t (&a
             v[2] += lo_bf(bw[1]);
             v[3] += hi_bf(bw[1]);
           }
-          if constexpr (EPI == Epi::kBiasResid) {
+          if constexpr (EPI == Epi::kBiasResid || EPI == Epi::kResid) {
             const u32x2_t rw = *reinterpret_cast<const u32x2_t *>(p.R + off);
             v[0] += lo_bf(rw[0]);
             v[1] += hi_bf(rw[0]);
@@ -184,7 +184,7 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
         const f32x4_t b = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc + 4);
         float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
         const size_t off = static_cast<size_t>(gm) * p.ldy + gn;
-        if constexpr (EPI == Epi::kBiasResid) {
+        if constexpr (EPI == Epi::kBiasResid || EPI == Epi::kResid) {
           const u32x4_t rw = ldg16(p.R + off);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -923,6 +923,8 @@ bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s) {
       return launch_lds<false, false, Epi::kBiasResid>(a, s) || launch_any<false, false, Epi::kBiasResid>(a, s);
     case Epi::kBiasGelu:
       return launch_lds<false, false, Epi::kBiasGelu>(a, s) || launch_any<false, false, Epi::kBiasGelu>(a, s);
+    case Epi::kPlain:
+      return launch_lds<false, false, Epi::kPlain>(a, s) || launch_any<false, false, Epi::kPlain>(a, s);
     default: return false;
   }
 }
@@ -933,6 +935,8 @@ bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s) {
       return launch_lds<false, true, Epi::kPlain>(a, s) || launch_any<false, true, Epi::kPlain>(a, s);
     case Epi::kGeluGrad:
       return launch_lds<false, true, Epi::kGeluGrad>(a, s) || launch_any<false, true, Epi::kGeluGrad>(a, s);
+    case Epi::kResid:
+      return launch_lds<false, true, Epi::kResid>(a, s) || launch_any<false, true, Epi::kResid>(a, s);
     default: return false;
   }
 }

@@ -27,6 +27,7 @@ enum class Epi : int {
   kGeluGrad = 3,   // Y = acc * GELU'(U[m, n])                (bf16 out)
   kPlain = 4,      // Y = acc                                 (bf16 out)
   kF32 = 5,        // Wf (+)= acc; optional fused db         (fp32 out)
+  kResid = 6,      // Y = acc + R[m, n]                       (bf16 out)
 };
 
 struct GemmArgs {
@@ -51,6 +52,14 @@ bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s);
 bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s);
 // Weight gradient: A(m, k) = dY[k, m], B(n, k) = X[k, n] (contraction over tokens).
 bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s);
+
+// ---- QK normalisation (LayerNorm of every query and key vector over head_dim)
+bool launch_qk_norm_fwd(int M, int heads, int d, const bf16_t *qkv, const bf16_t *qg, const bf16_t *qb,
+                        const bf16_t *kg, const bf16_t *kb, float eps, bf16_t *qkvn, float *stats, hipStream_t s);
+size_t qk_norm_bwd_ws_bytes(int M, int heads, int d);
+bool launch_qk_norm_bwd(int M, int heads, int d, const bf16_t *dqkvn, const bf16_t *qkv, const float *stats,
+                        const bf16_t *qg, const bf16_t *kg, bf16_t *dqkv, float *dqg, float *dqb, float *dkg,
+                        float *dkb, int accumulate, float *part, hipStream_t s);
 
 // ---- Attention
 bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s);

@@ -57,6 +57,35 @@ def layer_inputs(cfg, seed=0, std=0.02, with_dout=True):
     return x, params, dout
 
 
+PPARAM_ORDER = ("ln_g", "ln_b", "w_qkv", "qn_g", "qn_b", "kn_g", "kn_b", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2")
+
+
+def parallel_param_shapes(hidden, heads, head_dim, mlp):
+    A = heads * head_dim
+    return {"ln_g": (hidden,), "ln_b": (hidden,), "w_qkv": (3 * A, hidden), "qn_g": (head_dim,),
+            "qn_b": (head_dim,), "kn_g": (head_dim,), "kn_b": (head_dim,), "w_o": (hidden, A), "b_o": (hidden,),
+            "w_1": (mlp, hidden), "b_1": (mlp,), "w_2": (hidden, mlp), "b_2": (hidden,)}
+
+
+def parallel_block_inputs(cfg, seed=0, std=0.02):
+    """(x, params, dout) for the ViT-22B-style block, bfloat16 CPU tensors,
+    drawn like layer_inputs: x, then the parameters in PPARAM_ORDER (the
+    three LayerNorm scales 1 + N(0, std^2), everything else N(0, std^2)),
+    then dout."""
+    g = torch.Generator().manual_seed(seed)
+    M, H = cfg["batch"] * cfg["seq"], cfg["hidden"]
+
+    def normal(shape, s=1.0, mean=0.0):
+        t = torch.randn(shape, generator=g, dtype=torch.float32)
+        return (t * s + mean).to(torch.bfloat16)
+
+    x = normal((M, H))
+    shapes = parallel_param_shapes(H, cfg["heads"], cfg["head_dim"], cfg["mlp"])
+    params = {n: normal(shapes[n], std, 1.0 if n in ("ln_g", "qn_g", "kn_g") else 0.0) for n in PPARAM_ORDER}
+    dout = normal((M, H))
+    return x, params, dout
+
+
 def random_bf16(shape, seed, scale=1.0):
     """A seeded N(0, scale^2) tensor rounded to bfloat16 (CPU)."""
     g = torch.Generator().manual_seed(seed)

@@ -73,6 +73,22 @@ def test_saved_layout_is_aligned_and_disjoint(cfg):
     assert spans[-1][1] <= lay["total"]
 
 
+@pytest.mark.parametrize("cfg", [VIT22B, VIT_TINY])
+def test_parallel_saved_layout_is_aligned_and_disjoint(cfg):
+    lay = B.parallel_saved_layout(cfg)
+    M, nh = cfg["batch"] * cfg["seq"], cfg["heads"]
+    H, A, F = cfg["hidden"], nh * cfg["head_dim"], cfg["mlp"]
+    sizes = {"y": M * H * 2, "mean": M * 4, "rstd": M * 4, "qkv": M * 3 * A * 2, "qkvn": M * 3 * A * 2,
+             "qkstats": M * nh * 16, "o": M * A * 2, "lse": cfg["batch"] * nh * cfg["seq"] * 4, "h": M * H * 2,
+             "u": M * F * 2, "g": M * F * 2}
+    spans = sorted((lay[n], lay[n] + s) for n, s in sizes.items())
+    assert all(lay[n] % 256 == 0 for n in sizes)
+    assert all(a1 <= b0 for (_, a1), (b0, _) in zip(spans, spans[1:]))
+    assert spans[-1][1] <= lay["total"]
+    assert B.parallel_workspace_bytes(cfg) > 0
+    assert B.qk_norm_bwd_workspace_bytes(M, nh, cfg["head_dim"]) % (4 * 4 * cfg["head_dim"]) == 0
+
+
 def test_workspace_sizes():
     assert B.layer_workspace_bytes(VIT22B) > 0
     for rows, cols in ((2048, 6144), (10, 192), (6304, 768), (1, 8)):
@@ -111,7 +127,12 @@ def test_null_and_misaligned_pointers_are_rejected():
     assert _status("enc_ln_fwd", 4, 64, ctypes.c_void_p(FAKE + 2), p, p, ctypes.c_float(1e-6), p, p, p, s) \
         == B.ENC_ERR_ALIGN
     assert b"not 16-byte aligned" in B.lib().enc_last_error()
-    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, z, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, p, z, s) == B.ENC_ERR_INVALID  # b_qkv may be NULL, qkv not
+    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, ctypes.c_void_p(FAKE + 4), p, s) == B.ENC_ERR_ALIGN
+    assert _status("enc_qk_norm_fwd", 4, 2, 64, p, p, p, z, p, ctypes.c_float(1e-6), p, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_qk_norm_fwd", 4, 2, 96, p, p, p, p, p, ctypes.c_float(1e-6), p, p, s) \
+        == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_qkv_bwd_data_add", 8, 64, 64, p, p, z, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_attn_fwd", 1, 8, 1, 64, p, z, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, z, z, 0, s) == B.ENC_ERR_INVALID
     # db may be NULL, but a misaligned db is an error
