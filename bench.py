@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--fit-config", default="vit22b_tp8",
                     help="a second workload whose chain is timed briefly and packed into the synthetic "
                          "TP-bubble trace beside the main one ('' to skip)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip timing the ViT-22B-style parallel block at the same shape")
+    ap.add_argument("--no-corun", action="store_true",
+                    help="skip the co-run measurement (encoder chain beside a GEMM load on a second stream)")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-only and device-copy reference kernels")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -313,6 +317,122 @@ def time_chain(chain, steps, warmup):
             for i, n in enumerate(names)}
 
 
+def time_parallel_block(cfg, dev, steps=10, warmup=3):
+    """Forward+backward of the ViT-22B-style parallel block (composite entry
+    points) at the same shape, plus its two QK-norm kernels on their own."""
+    from paper_2408_03505_amd import binding as B
+    from paper_2408_03505_amd.synthetic import PPARAM_ORDER, parallel_block_inputs
+    import oracle
+    x, p, d = parallel_block_inputs(cfg, seed=0)
+    gx, gd = x.to(dev), d.to(dev)
+    gp = {n: p[n].to(dev) for n in PPARAM_ORDER}
+    out, saved = B.encoder_parallel_fwd(cfg, gp, gx)
+    dx, grads = B.encoder_parallel_bwd(cfg, gp, gx, saved, gd)
+    ws = torch.empty(B.parallel_workspace_bytes(cfg), dtype=torch.uint8, device=dev)
+
+    def step():
+        B.encoder_parallel_fwd(cfg, gp, gx, out=out, saved=saved)
+        B.encoder_parallel_bwd(cfg, gp, gx, saved, gd, grads=grads, dx=dx, ws=ws)
+
+    def p50_ms(fn, n):
+        ts = []
+        for _ in range(n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = p50_ms(step, steps)
+    flops = 3 * oracle.layer_flops(cfg)
+    v = B.parallel_saved_views(cfg, saved)
+    nh, dd, M = cfg["heads"], cfg["head_dim"], cfg["batch"] * cfg["seq"]
+    qkvn, st = v["qkvn"].clone(), v["qkstats"].clone()
+    fwd = lambda: B.enc_qk_norm_fwd(nh, dd, v["qkv"], gp["qn_g"], gp["qn_b"], gp["kn_g"], gp["kn_b"],  # noqa: E731
+                                    cfg["ln_eps"], qkvn=qkvn, stats=st)
+    dq = torch.empty_like(qkvn)
+    qg = {n: torch.empty(dd, dtype=torch.float32, device=dev) for n in ("qn_g", "qn_b", "kn_g", "kn_b")}
+    bwd = lambda: B.enc_qk_norm_bwd(nh, dd, qkvn, v["qkv"], st, gp["qn_g"], gp["kn_g"], dqkv=dq,  # noqa: E731
+                                    grads=qg)
+    for f in (fwd, bwd):
+        f()
+    fwd_us, bwd_us = p50_ms(fwd, 20) * 1e3, p50_ms(bwd, 20) * 1e3
+    A = nh * dd
+    fwd_bytes = M * 3 * A * 2 * 2 + M * nh * 16            # read qkv, write qkvn, stats
+    bwd_bytes = M * 3 * A * 2 * 2 + M * 2 * A * 2 + M * nh * 16  # read dqkvn, q/k, stats; write dqkv
+    return {"ms_per_step": round(ms, 4), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "qk_norm_fwd": {"p50_us": round(fwd_us, 2), "gbs": round(fwd_bytes / (fwd_us * 1e-6) / 1e9, 1)},
+            "qk_norm_bwd": {"p50_us": round(bwd_us, 2), "gbs": round(bwd_bytes / (bwd_us * 1e-6) / 1e9, 1)},
+            "note": "ViT-22B-style block (shared LN, parallel branches, QK LayerNorm, no QKV bias) at the same "
+                    "shape; composite entry points, p50 of 10 steps; flops counted as for the sequential layer"}
+
+
+def corun(chain, p50_alone, dev, steps=5, n=8192):
+    """The encoder chain on one stream while a loop of n x n x n bf16 GEMMs
+    (torch.matmul, standing in for the LLM's computation) runs on another;
+    per-kernel p50 under load against p50_alone, and the load's own rate
+    alone and beside the chain.  Both streams have the default priority."""
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    load, enc = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    gemm_flops = 2.0 * n ** 3
+
+    def run_load(k):
+        with torch.cuda.stream(load):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(k):
+                torch.matmul(a, b, out=c)
+            e1.record()
+        return e0, e1
+
+    e0, e1 = run_load(3)
+    torch.cuda.synchronize()
+    e0, e1 = run_load(20)
+    torch.cuda.synchronize()
+    load_alone = 20 * gemm_flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    names = [nm for nm, _ in chain.kernels]
+    step_ms_alone = sum(p50_alone.values()) / 1e3
+    # enough load to outlast the chain even if sharing the GPU slows it eightfold
+    k_load = max(8, int(8.0 * steps * step_ms_alone / max(1e-3, gemm_flops / (load_alone * 1e12) * 1e3)))
+    torch.cuda.synchronize()
+    l0, l1 = run_load(k_load)
+    ev = []
+    with torch.cuda.stream(enc):
+        s0 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(steps):
+            row = []
+            for _, fn in chain.kernels:
+                k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                k0.record()
+                fn()
+                k1.record()
+                row.append((k0, k1))
+            ev.append(row)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s1.record()
+    torch.cuda.synchronize()
+    per = {nm: float(np.median([ev[k][i][0].elapsed_time(ev[k][i][1]) * 1e3 for k in range(steps)]))
+           for i, nm in enumerate(names)}
+    enc_ms = s0.elapsed_time(s1) / steps
+    load_busy = k_load * gemm_flops / (l0.elapsed_time(l1) * 1e-3) / 1e12
+    covered = l0.elapsed_time(s0) >= 0 and s1.elapsed_time(l1) >= 0  # the load spans the whole chain
+    return {"load": f"bf16 GEMM {n}x{n}x{n} (torch.matmul) looped on a second stream, {k_load} launches",
+            "load_covers_encoder": bool(covered),
+            "encoder_step_ms_alone": round(step_ms_alone, 4), "encoder_step_ms_corun": round(enc_ms, 4),
+            "step_slowdown": round(enc_ms / step_ms_alone, 3),
+            "kernel_slowdown": {nm: round(per[nm] / p50_alone[nm], 2) for nm in names},
+            "load_tflops_alone": round(load_alone, 1), "load_tflops_corun": round(load_busy, 1)}
+
+
 class Chain:
     """Preallocated buffers and the kernel-by-kernel layer step."""
 
@@ -522,6 +642,10 @@ def main():
         fit[args.fit_config]["p50_us"] = {n: round(v, 2) for n, v in fp50.items()}
         del fchain
     res["bubble_fit"] = fit
+    if not args.no_corun:
+        res["corun"] = corun(chain, p50, dev)
+    if not args.no_variants:
+        res["variants"] = {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)}
     if not args.no_ceilings:
         ceil = measure_ceilings(dev)
         res["ceilings"] = ceil

@@ -8,7 +8,8 @@
 // over four xor-shuffles.  The backward writes dq, dk (LayerNorm backward)
 // and dv (copied), and reduces the affine gradients in a fixed order: every
 // lane sums its elements over the pairs its group visits, the 16 groups of a
-// block are added in LDS, and a second kernel adds the blocks' partials.
+// block are added in LDS, and a second kernel adds the blocks' partials
+// (one block per gradient element, fixed-order tree).
 #include <math.h>
 
 #include "common.hpp"
@@ -161,17 +162,26 @@ __global__ __launch_bounds__(256) void qk_norm_bwd_kernel(int pairs, int heads, 
   }
 }
 
+// One block per affine-gradient element: strided partial sums over the
+// blocks' partials, then a fixed-order tree in LDS (deterministic).
 __global__ __launch_bounds__(256) void qk_norm_reduce_kernel(int blocks, int D, const float *__restrict__ part,
                                                              float *__restrict__ dqg, float *__restrict__ dqb,
                                                              float *__restrict__ dkg, float *__restrict__ dkb,
                                                              int accumulate) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= 4 * D) return;
-  const int k = t / D, e = t % D;
+  __shared__ float red[256];
+  const int k = blockIdx.x / D, e = blockIdx.x % D;
   float s = 0.f;
-  for (int b = 0; b < blocks; ++b) s += part[(static_cast<size_t>(b) * 4 + k) * D + e];
-  float *out = k == 0 ? dqg : k == 1 ? dqb : k == 2 ? dkg : dkb;
-  out[e] = accumulate ? out[e] + s : s;
+  for (int b = threadIdx.x; b < blocks; b += 256) s += part[(static_cast<size_t>(b) * 4 + k) * D + e];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    float *out = k == 0 ? dqg : k == 1 ? dqb : k == 2 ? dkg : dkb;
+    out[e] = accumulate ? out[e] + red[0] : red[0];
+  }
 }
 
 int bwd_blocks(int M, int heads) {
@@ -195,8 +205,8 @@ void bwd_d(int M, int heads, const bf16_t *dqkvn, const bf16_t *qkv, const float
   const int nb = bwd_blocks(M, heads);
   hipLaunchKernelGGL(qk_norm_bwd_kernel<D>, dim3(nb), dim3(256), 0, s, M * heads, heads, dqkvn, qkv, stats, qg, kg,
                      dqkv, part);
-  hipLaunchKernelGGL(qk_norm_reduce_kernel, dim3((4 * D + 255) / 256), dim3(256), 0, s, nb, D, part, dqg, dqb, dkg,
-                     dkb, accumulate);
+  hipLaunchKernelGGL(qk_norm_reduce_kernel, dim3(4 * D), dim3(256), 0, s, nb, D, part, dqg, dqb, dkg, dkb,
+                     accumulate);
 }
 
 }  // namespace
