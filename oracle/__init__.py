@@ -7,6 +7,6 @@ from .encoder_layer import *  # noqa: F401,F403
 from .encoder_layer import __all__ as _layer_all
 from .parallel_layer import *  # noqa: F401,F403
 from .parallel_layer import __all__ as _parallel_all
-from . import schedule  # noqa: F401
+from . import schedule, vit_encoder  # noqa: F401
 
-__all__ = list(_layer_all) + list(_parallel_all) + ["schedule"]
+__all__ = list(_layer_all) + list(_parallel_all) + ["schedule", "vit_encoder"]
