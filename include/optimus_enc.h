@@ -350,6 +350,58 @@ int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv,
                          const enc_bf16 *w_qkv, const enc_bf16 *addend,
                          enc_bf16 *dy, enc_stream_t stream);
 
+/* ------------------------------------------------------------ whole encoder
+ *
+ * The encoders of the paper are ViTs (Appendix A): a patch embedding, a
+ * stack of encoder layers and a final LayerNorm.  An image of side img cut
+ * into p x p patches gives N = (img_h/p)(img_w/p) tokens, plus one class
+ * token when has_cls (224/16 -> 196 + 1 = 197; 224/14 -> 256).
+ *
+ * Patch embedding: the stride-p convolution as a matrix product,
+ *   patches[b*N + n, c*p*p + i*p + j] = images[b, c, py*p + i, px*p + j]
+ *   (n = py*(img_w/p) + px; images [B, C, img_h, img_w] bf16),
+ *   tok = patches * w_pe^T + b_pe,
+ *   x0[b*S + s] = (has_cls and s == 0 ? cls : tok[b*N + s - has_cls]) + pos[s],
+ * with S = N + has_cls.  Kp = C*p*p rounded up to a multiple of 8: patches
+ * is [B*N, Kp] and w_pe is [hidden, Kp] whose columns C*p*p .. Kp-1 must be
+ * zero (they are written zero in patches).  cls [hidden] (only with
+ * has_cls), pos [S, hidden], b_pe [hidden].  ws: with has_cls,
+ * enc_patch_embed_workspace_bytes (the tokens before the class token is
+ * placed); without, none (the tokens are x0's rows). */
+int enc_patch_embed_workspace_bytes(int batch, int channels, int img_h, int img_w, int patch, int hidden,
+                                    int has_cls, size_t *bytes);
+int enc_patch_embed_fwd(int batch, int channels, int img_h, int img_w, int patch, int hidden, int has_cls,
+                        const enc_bf16 *images, const enc_bf16 *w_pe, const enc_bf16 *b_pe, const enc_bf16 *cls,
+                        const enc_bf16 *pos, enc_bf16 *patches, enc_bf16 *x0, void *ws, size_t ws_bytes,
+                        enc_stream_t stream);
+/* Parameter gradients of the patch embedding from dx0 [B*S, hidden] and the
+ * forward's patches: dw_pe [hidden, Kp], db_pe [hidden], dpos [S, hidden]
+ * (sum over the batch in order), dcls [hidden] (only with has_cls) -- all
+ * fp32, overwritten or (accumulate=1) added.  The images get no gradient.
+ * ws: as for the forward. */
+int enc_patch_embed_bwd(int batch, int channels, int img_h, int img_w, int patch, int hidden, int has_cls,
+                        const enc_bf16 *dx0, const enc_bf16 *patches, float *dw_pe, float *db_pe, float *dcls,
+                        float *dpos, int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream);
+
+/* A stack of `layers` sequential encoder layers (params[layers], each as for
+ * encoder_layer_fwd) followed by a final LayerNorm (lnf_g, lnf_b):
+ * out = LN(layer_{L-1}(... layer_0(x0))).  saved (enc_stack_saved_bytes)
+ * holds every layer's output (the next layer's input), every layer's saved
+ * tensors and the final LayerNorm's statistics. */
+int enc_stack_saved_bytes(const enc_cfg_t *cfg, int layers, size_t *bytes);
+int enc_stack_workspace_bytes(const enc_cfg_t *cfg, int layers, size_t *bytes);
+int encoder_stack_fwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params,
+                      const enc_bf16 *lnf_g, const enc_bf16 *lnf_b, const enc_bf16 *x0,
+                      enc_bf16 *out, void *saved, enc_stream_t stream);
+/* Backward of encoder_stack_fwd: dx0 and the gradients of every layer
+ * (grads[layers]) and of the final LayerNorm; accumulate as for
+ * encoder_layer_bwd.  ws: enc_stack_workspace_bytes. */
+int encoder_stack_bwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params,
+                      const enc_bf16 *lnf_g, const enc_bf16 *x0, const void *saved,
+                      const enc_bf16 *dout, enc_bf16 *dx0, const enc_grads_t *grads,
+                      float *dlnf_g, float *dlnf_b, int accumulate, void *ws,
+                      size_t ws_bytes, enc_stream_t stream);
+
 /* ---- Kernel-to-bubble packing (host code, no GPU)
  *
  * The bubble scheduler's ScheduleKernels step (§4.2, fine-grained bubble

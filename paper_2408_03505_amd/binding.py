@@ -102,6 +102,13 @@ _SIGS = {
     "enc_qk_norm_bwd_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
     "enc_qk_norm_bwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_qkv_bwd_data_add": [_i, _i, _i, _p, _p, _p, _p, _p],
+    "enc_patch_embed_workspace_bytes": [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
+    "enc_patch_embed_fwd": [_i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_patch_embed_bwd": [_i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_stack_saved_bytes": [_PCFG, _i, ctypes.POINTER(_sz)],
+    "enc_stack_workspace_bytes": [_PCFG, _i, ctypes.POINTER(_sz)],
+    "encoder_stack_fwd": [_PCFG, _i, _p, _p, _p, _p, _p, _p, _p],
+    "encoder_stack_bwd": [_PCFG, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_calib_copy": [_p, _p, _sz, _p],
 }
 
@@ -665,3 +672,133 @@ def enc_qkv_bwd_data_add(dqkv, w_qkv, addend, dy=None, stream=None):
     dy = _out(dy, "dy", (M, H), dqkv)
     _call("enc_qkv_bwd_data_add", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(addend), _ptr(dy), _stream(stream))
     return dy
+
+
+# ---------------------------------------------------------------- whole encoder
+
+def patch_kp(channels, patch):
+    """Columns of the patch matrix: C*p*p rounded up to a multiple of 8."""
+    return (channels * patch * patch + 7) // 8 * 8
+
+
+def patch_embed_workspace_bytes(batch, channels, img_h, img_w, patch, hidden, has_cls):
+    n = ctypes.c_size_t()
+    _call("enc_patch_embed_workspace_bytes", batch, channels, img_h, img_w, patch, hidden, int(bool(has_cls)),
+          ctypes.byref(n))
+    return n.value
+
+
+def enc_patch_embed_fwd(images, patch, w_pe, b_pe, pos, cls=None, patches=None, x0=None, ws=None, stream=None):
+    """images [B, C, H_img, W_img] bf16; w_pe [hidden, Kp] (zero beyond C*p*p).
+    Returns (x0 [B*S, hidden], patches [B*N, Kp])."""
+    B, C, ih, iw = images.shape
+    hidden = w_pe.shape[0]
+    kp = patch_kp(C, patch)
+    N = (ih // patch) * (iw // patch)
+    has_cls = cls is not None
+    S = N + int(has_cls)
+    _check(images, "images", (B, C, ih, iw))
+    _check(w_pe, "w_pe", (hidden, kp))
+    _check(b_pe, "b_pe", (hidden,))
+    _check(pos, "pos", (S, hidden))
+    if has_cls:
+        _check(cls, "cls", (hidden,))
+    patches = _out(patches, "patches", (B * N, kp), images)
+    x0 = _out(x0, "x0", (B * S, hidden), images)
+    need = patch_embed_workspace_bytes(B, C, ih, iw, patch, hidden, has_cls)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=images.device)
+    _call("enc_patch_embed_fwd", B, C, ih, iw, patch, hidden, int(has_cls), _ptr(images), _ptr(w_pe), _ptr(b_pe),
+          _ptr(cls), _ptr(pos), _ptr(patches), _ptr(x0), _ptr(ws), ws.numel() if ws is not None else 0,
+          _stream(stream))
+    return x0, patches
+
+
+def enc_patch_embed_bwd(images_shape, patch, dx0, patches, has_cls, grads=None, accumulate=False, ws=None,
+                        stream=None):
+    """Returns a dict of fp32 gradients w_pe [hidden, Kp], b_pe, pos [S, hidden], cls (with has_cls)."""
+    B, C, ih, iw = images_shape
+    kp = patch_kp(C, patch)
+    N = (ih // patch) * (iw // patch)
+    S = N + int(bool(has_cls))
+    hidden = dx0.shape[1]
+    _check(dx0, "dx0", (B * S, hidden))
+    _check(patches, "patches", (B * N, kp))
+    shapes = {"w_pe": (hidden, kp), "b_pe": (hidden,), "pos": (S, hidden)}
+    if has_cls:
+        shapes["cls"] = (hidden,)
+    if grads is None:
+        if accumulate:
+            raise ValueError("accumulate=True needs existing grads")
+        grads = {k: torch.empty(v, dtype=torch.float32, device=dx0.device) for k, v in shapes.items()}
+    for k, v in shapes.items():
+        _check(grads[k], "d" + k, v, torch.float32)
+    need = patch_embed_workspace_bytes(B, C, ih, iw, patch, hidden, has_cls)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=dx0.device)
+    _call("enc_patch_embed_bwd", B, C, ih, iw, patch, hidden, int(bool(has_cls)), _ptr(dx0), _ptr(patches),
+          _ptr(grads["w_pe"]), _ptr(grads["b_pe"]), _ptr(grads.get("cls")), _ptr(grads["pos"]),
+          1 if accumulate else 0, _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
+    return grads
+
+
+def stack_saved_bytes(cfg, layers):
+    n = ctypes.c_size_t()
+    c = make_cfg(cfg)
+    _call("enc_stack_saved_bytes", ctypes.byref(c), layers, ctypes.byref(n))
+    return n.value
+
+
+def stack_workspace_bytes(cfg, layers):
+    n = ctypes.c_size_t()
+    c = make_cfg(cfg)
+    _call("enc_stack_workspace_bytes", ctypes.byref(c), layers, ctypes.byref(n))
+    return n.value
+
+
+def encoder_stack_fwd(cfg, layer_params, lnf_g, lnf_b, x0, out=None, saved=None, stream=None):
+    """layer_params: list of per-layer parameter dicts (PARAM_ORDER).  Returns (out, saved)."""
+    L = len(layer_params)
+    M, H = cfg["batch"] * cfg["seq"], cfg["hidden"]
+    _check(x0, "x0", (M, H))
+    _check(lnf_g, "lnf_g", (H,))
+    _check(lnf_b, "lnf_b", (H,))
+    out = _out(out, "out", (M, H), x0)
+    saved = _out(saved, "saved", (stack_saved_bytes(cfg, L),), x0, torch.uint8)
+    arr = (EncParams * L)(*[_params_struct(cfg, p) for p in layer_params])
+    c = make_cfg(cfg)
+    _call("encoder_stack_fwd", ctypes.byref(c), L, ctypes.cast(arr, _p), _ptr(lnf_g), _ptr(lnf_b), _ptr(x0),
+          _ptr(out), _ptr(saved), _stream(stream))
+    return out, saved
+
+
+def encoder_stack_bwd(cfg, layer_params, lnf_g, x0, saved, dout, grads=None, lnf_grads=None, dx0=None,
+                      accumulate=False, ws=None, stream=None):
+    """Returns (dx0, per-layer grads list, (dlnf_g, dlnf_b))."""
+    L = len(layer_params)
+    M, H = cfg["batch"] * cfg["seq"], cfg["hidden"]
+    _check(x0, "x0", (M, H))
+    _check(dout, "dout", (M, H))
+    _check(saved, "saved", (stack_saved_bytes(cfg, L),), torch.uint8)
+    dx0 = _out(dx0, "dx0", (M, H), x0)
+    shapes = param_shapes(cfg)
+    if grads is None:
+        if accumulate:
+            raise ValueError("accumulate=True needs existing grads")
+        grads = [{n: torch.empty(shapes[n], dtype=torch.float32, device=x0.device) for n in PARAM_ORDER}
+                 for _ in range(L)]
+        lnf_grads = tuple(torch.empty(H, dtype=torch.float32, device=x0.device) for _ in range(2))
+    for g in grads:
+        for n in PARAM_ORDER:
+            _check(g[n], "d" + n, shapes[n], torch.float32)
+    for t in lnf_grads:
+        _check(t, "dlnf", (H,), torch.float32)
+    if ws is None:
+        ws = torch.empty(stack_workspace_bytes(cfg, L), dtype=torch.uint8, device=x0.device)
+    arr = (EncParams * L)(*[_params_struct(cfg, p) for p in layer_params])
+    garr = (EncGrads * L)(*[EncGrads(*[_ptr(g[n]) for n in PARAM_ORDER]) for g in grads])
+    c = make_cfg(cfg)
+    _call("encoder_stack_bwd", ctypes.byref(c), L, ctypes.cast(arr, _p), _ptr(lnf_g), _ptr(x0), _ptr(saved),
+          _ptr(dout), _ptr(dx0), ctypes.cast(garr, _p), _ptr(lnf_grads[0]), _ptr(lnf_grads[1]),
+          1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream))
+    return dx0, grads, lnf_grads

@@ -318,6 +318,55 @@ int check_pgrads(const char *fn, const enc_pgrads_t *g) {
   return c.code;
 }
 
+int patch_dims(const char *fn, int B, int C, int ih, int iw, int p, int H, int has_cls, int *N, int *S, int *Kp) {
+  int r = check_dims(fn, {B, C, ih, iw, p, H});
+  if (r) return r;
+  if (has_cls != 0 && has_cls != 1) return fail(ENC_ERR_INVALID, "%s: has_cls must be 0 or 1", fn);
+  if (ih % p || iw % p) return fail(ENC_ERR_UNSUPPORTED, "%s: image sides must be multiples of the patch", fn);
+  if (H % 8) return fail(ENC_ERR_UNSUPPORTED, "%s: hidden must be a multiple of 8", fn);
+  *N = (ih / p) * (iw / p);
+  *S = *N + has_cls;
+  *Kp = (C * p * p + 7) / 8 * 8;
+  const long M = static_cast<long>(B) * *N;
+  if (M * *Kp >= kMaxElems || static_cast<long>(B) * *S * H >= kMaxElems ||
+      static_cast<long>(B) * C * ih * iw >= kMaxElems)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+struct StackLayout {
+  size_t x_step, layer_step, layers_off, mean, rstd, total;
+};
+
+StackLayout stack_layout(const enc_cfg_t *c, int layers) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  enc_saved_layout_t L;
+  saved_layout(c, &L);
+  StackLayout s{};
+  s.x_step = round256(M * c->hidden * 2);
+  s.layer_step = L.total;
+  s.layers_off = s.x_step * layers;
+  s.mean = s.layers_off + s.layer_step * layers;
+  s.rstd = s.mean + round256(M * 4);
+  s.total = s.rstd + round256(M * 4);
+  return s;
+}
+
+struct StackWs {
+  size_t layer, dx_a, dx_b, ln_part, total;
+};
+
+StackWs stack_ws(const enc_cfg_t *c) {
+  const size_t M = static_cast<size_t>(c->batch) * c->seq;
+  StackWs w{};
+  w.layer = 0;
+  w.dx_a = round256(bwd_layout(c).total);
+  w.dx_b = w.dx_a + round256(M * c->hidden * 2);
+  w.ln_part = w.dx_b + round256(M * c->hidden * 2);
+  w.total = w.ln_part + round256(ln_bwd_ws_bytes(static_cast<int>(M), c->hidden));
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -802,6 +851,156 @@ int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   okk = okk && launch_ln_bwd(M, H, dy, x, mean, rstd, p.ln_g, dout, dx, gr.ln_g, gr.ln_b, acc, ln_part, s);
   if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
   return launched(fn);
+}
+
+// ------------------------------------------------------------ patch embedding and layer stack
+
+int enc_patch_embed_workspace_bytes(int batch, int channels, int img_h, int img_w, int patch, int hidden, int has_cls,
+                                    size_t *bytes) {
+  const char *fn = "enc_patch_embed_workspace_bytes";
+  int N, S, Kp;
+  int r = patch_dims(fn, batch, channels, img_h, img_w, patch, hidden, has_cls, &N, &S, &Kp);
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = has_cls ? static_cast<size_t>(batch) * N * hidden * 2 : 0;
+  return ok();
+}
+
+int enc_patch_embed_fwd(int batch, int channels, int img_h, int img_w, int patch, int hidden, int has_cls,
+                        const enc_bf16 *images, const enc_bf16 *w_pe, const enc_bf16 *b_pe, const enc_bf16 *cls,
+                        const enc_bf16 *pos, enc_bf16 *patches, enc_bf16 *x0, void *ws, size_t ws_bytes,
+                        enc_stream_t stream) {
+  const char *fn = "enc_patch_embed_fwd";
+  int N, S, Kp;
+  int r = patch_dims(fn, batch, channels, img_h, img_w, patch, hidden, has_cls, &N, &S, &Kp);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(images, "images").req(w_pe, "w_pe").req(b_pe, "b_pe").req(pos, "pos").req(patches, "patches").req(x0, "x0");
+  if (has_cls) c.req(cls, "cls").req(ws, "ws");
+  if (c.code) return c.code;
+  const size_t need = has_cls ? static_cast<size_t>(batch) * N * hidden * 2 : 0;
+  if (ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  const hipStream_t s = as_stream(stream);
+  bf16_t *tok = has_cls ? static_cast<bf16_t *>(ws) : x0;  // without a class token the tokens are x0's rows
+  bool okk = launch_patchify(batch, channels, img_h, img_w, patch, Kp, images, patches, s);
+  okk = okk && gemm_fwd(batch * N, hidden, Kp, patches, w_pe, b_pe, nullptr, tok, nullptr, Epi::kBias, s);
+  okk = okk && launch_patch_assemble(batch, N, S, hidden, has_cls, tok, cls, pos, x0, s);
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+int enc_patch_embed_bwd(int batch, int channels, int img_h, int img_w, int patch, int hidden, int has_cls,
+                        const enc_bf16 *dx0, const enc_bf16 *patches, float *dw_pe, float *db_pe, float *dcls,
+                        float *dpos, int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "enc_patch_embed_bwd";
+  int N, S, Kp;
+  int r = patch_dims(fn, batch, channels, img_h, img_w, patch, hidden, has_cls, &N, &S, &Kp);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(dx0, "dx0").req(patches, "patches").req(dw_pe, "dw_pe").req(db_pe, "db_pe").req(dpos, "dpos");
+  if (has_cls) c.req(dcls, "dcls").req(ws, "ws");
+  if (c.code) return c.code;
+  const size_t need = has_cls ? static_cast<size_t>(batch) * N * hidden * 2 : 0;
+  if (ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  const hipStream_t s = as_stream(stream);
+  const int acc = accumulate ? 1 : 0;
+  bool okk = launch_patch_pos_grad(batch, S, hidden, dx0, dpos, has_cls ? dcls : nullptr, acc, s);
+  const bf16_t *dtok = dx0;
+  if (has_cls) {
+    okk = okk && launch_patch_token_rows(batch, N, S, hidden, dx0, static_cast<bf16_t *>(ws), s);
+    dtok = static_cast<const bf16_t *>(ws);
+  }
+  okk = okk && gemm_wgrad(batch * N, hidden, Kp, dtok, patches, dw_pe, db_pe, acc, s);
+  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  return launched(fn);
+}
+
+int enc_stack_saved_bytes(const enc_cfg_t *cfg, int layers, size_t *bytes) {
+  const char *fn = "enc_stack_saved_bytes";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (layers <= 0) return fail(ENC_ERR_INVALID, "%s: layers must be positive", fn);
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = stack_layout(cfg, layers).total;
+  return ok();
+}
+
+int enc_stack_workspace_bytes(const enc_cfg_t *cfg, int layers, size_t *bytes) {
+  const char *fn = "enc_stack_workspace_bytes";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (layers <= 0) return fail(ENC_ERR_INVALID, "%s: layers must be positive", fn);
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = stack_ws(cfg).total;
+  return ok();
+}
+
+int encoder_stack_fwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params, const enc_bf16 *lnf_g,
+                      const enc_bf16 *lnf_b, const enc_bf16 *x0, enc_bf16 *out, void *saved, enc_stream_t stream) {
+  const char *fn = "encoder_stack_fwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (layers <= 0) return fail(ENC_ERR_INVALID, "%s: layers must be positive", fn);
+  if (!params) return fail(ENC_ERR_INVALID, "%s: params is NULL", fn);
+  for (int l = 0; l < layers; ++l)
+    if ((r = check_params(fn, &params[l]))) return r;
+  PtrCheck c(fn);
+  c.req(lnf_g, "lnf_g").req(lnf_b, "lnf_b").req(x0, "x0").req(out, "out").req(saved, "saved");
+  if (c.code) return c.code;
+  const StackLayout L = stack_layout(cfg, layers);
+  const int M = cfg->batch * cfg->seq;
+  const enc_bf16 *x = x0;
+  for (int l = 0; l < layers; ++l) {
+    enc_bf16 *y = at<enc_bf16>(saved, L.x_step * l);  // layer l's output = layer l+1's input
+    if ((r = encoder_layer_fwd(cfg, &params[l], x, y, at<char>(saved, L.layers_off + L.layer_step * l), nullptr, 0,
+                               stream)))
+      return r;
+    x = y;
+  }
+  if (!launch_ln_fwd(M, cfg->hidden, x, lnf_g, lnf_b, cfg->ln_eps, out, at<float>(saved, L.mean),
+                     at<float>(saved, L.rstd), as_stream(stream)))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+  return launched(fn);
+}
+
+int encoder_stack_bwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params, const enc_bf16 *lnf_g,
+                      const enc_bf16 *x0, const void *saved, const enc_bf16 *dout, enc_bf16 *dx0,
+                      const enc_grads_t *grads, float *dlnf_g, float *dlnf_b, int accumulate, void *ws,
+                      size_t ws_bytes, enc_stream_t stream) {
+  const char *fn = "encoder_stack_bwd";
+  int r = check_cfg(fn, cfg);
+  if (r) return r;
+  if (layers <= 0) return fail(ENC_ERR_INVALID, "%s: layers must be positive", fn);
+  if (!params || !grads) return fail(ENC_ERR_INVALID, "%s: params or grads is NULL", fn);
+  for (int l = 0; l < layers; ++l) {
+    if ((r = check_params(fn, &params[l]))) return r;
+    if ((r = check_grads(fn, &grads[l]))) return r;
+  }
+  PtrCheck c(fn);
+  c.req(lnf_g, "lnf_g").req(x0, "x0").req(saved, "saved").req(dout, "dout").req(dx0, "dx0");
+  c.req(dlnf_g, "dlnf_g").req(dlnf_b, "dlnf_b").req(ws, "ws");
+  if (c.code) return c.code;
+  const StackWs W = stack_ws(cfg);
+  if (ws_bytes < W.total) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, W.total);
+  const StackLayout L = stack_layout(cfg, layers);
+  const int M = cfg->batch * cfg->seq;
+  const hipStream_t s = as_stream(stream);
+  enc_bf16 *bufs[2] = {at<enc_bf16>(ws, W.dx_a), at<enc_bf16>(ws, W.dx_b)};
+  const enc_bf16 *xL = at<enc_bf16>(saved, L.x_step * (layers - 1));
+  if (!launch_ln_bwd(M, cfg->hidden, dout, xL, at<float>(saved, L.mean), at<float>(saved, L.rstd), lnf_g, nullptr,
+                     bufs[0], dlnf_g, dlnf_b, accumulate ? 1 : 0, at<float>(ws, W.ln_part), s))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+  if ((r = launched(fn))) return r;
+  int cur = 0;
+  for (int l = layers - 1; l >= 0; --l) {
+    const enc_bf16 *xl = l == 0 ? x0 : at<enc_bf16>(saved, L.x_step * (l - 1));
+    enc_bf16 *dxl = l == 0 ? dx0 : bufs[cur ^ 1];
+    if ((r = encoder_layer_bwd(cfg, &params[l], xl, at<char>(saved, L.layers_off + L.layer_step * l), bufs[cur], dxl,
+                               &grads[l], accumulate, ws, W.dx_a, stream)))
+      return r;
+    cur ^= 1;
+  }
+  return ok();
 }
 
 // ------------------------------------------------------------ measurement helpers

@@ -67,6 +67,15 @@ size_t attn_bwd_ws_bytes(int B, int S, int heads);
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s);
 
+// ---- Patch embedding (images -> patch rows; tokens + class token + positions)
+bool launch_patchify(int B, int C, int img_h, int img_w, int p, int Kp, const bf16_t *images, bf16_t *patches,
+                     hipStream_t s);
+bool launch_patch_assemble(int B, int N, int S, int H, int has_cls, const bf16_t *tok, const bf16_t *cls,
+                           const bf16_t *pos, bf16_t *x0, hipStream_t s);
+bool launch_patch_pos_grad(int B, int S, int H, const bf16_t *dx0, float *dpos, float *dcls, int accumulate,
+                           hipStream_t s);
+bool launch_patch_token_rows(int B, int N, int S, int H, const bf16_t *dx0, bf16_t *dtok, hipStream_t s);
+
 // ---- Measurement reference kernels
 bool launch_calib_mfma(int blocks, int iters, float *out, hipStream_t s);
 bool launch_calib_copy(const void *src, void *dst, size_t bytes, hipStream_t s);

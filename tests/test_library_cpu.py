@@ -165,6 +165,28 @@ def test_calibration_arguments_are_checked():
 
 
 @no_gpu_only
+def test_patch_and_stack_arguments_are_checked():
+    p, z, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0), ctypes.c_void_p(0)
+    # image side not a multiple of the patch
+    assert _status("enc_patch_embed_fwd", 1, 3, 30, 28, 14, 64, 0, p, p, p, z, p, p, p, z, 0, s) \
+        == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_patch_embed_fwd", 1, 3, 28, 28, 14, 64, 2, p, p, p, p, p, p, p, p, 1 << 20, s) \
+        == B.ENC_ERR_INVALID
+    # a class token needs cls and a workspace
+    assert _status("enc_patch_embed_fwd", 1, 3, 28, 28, 14, 64, 1, p, p, p, z, p, p, p, p, 1 << 20, s) \
+        == B.ENC_ERR_INVALID
+    assert _status("enc_patch_embed_fwd", 1, 3, 28, 28, 14, 64, 1, p, p, p, p, p, p, p, p, 16, s) \
+        == B.ENC_ERR_WORKSPACE
+    assert B.patch_embed_workspace_bytes(2, 3, 224, 224, 16, 192, False) == 0
+    assert B.patch_embed_workspace_bytes(2, 3, 224, 224, 16, 192, True) == 2 * 196 * 192 * 2
+    assert B.patch_kp(3, 14) == 592 and B.patch_kp(3, 16) == 768
+    cfg = B.make_cfg(VIT_TINY)
+    assert _status("encoder_stack_fwd", ctypes.byref(cfg), 0, p, p, p, p, p, p, s) == B.ENC_ERR_INVALID
+    one = B.stack_saved_bytes(VIT_TINY, 1)
+    assert B.stack_saved_bytes(VIT_TINY, 4) > 3 * one and B.stack_workspace_bytes(VIT_TINY, 4) > 0
+
+
+@no_gpu_only
 def test_small_workspace_is_rejected():
     p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
     need = B.ln_bwd_workspace_bytes(16, 64)
