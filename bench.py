@@ -45,6 +45,9 @@ def parse():
                     help="skip timing the ViT-22B-style parallel block at the same shape")
     ap.add_argument("--no-corun", action="store_true",
                     help="skip the co-run measurement (encoder chain beside a GEMM load on a second stream)")
+    ap.add_argument("--encoder-layers", type=int, default=48,
+                    help="also time the whole encoder (patch embedding + this many layers + final LayerNorm) "
+                         "at the workload's shape; 0 skips it")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-only and device-copy reference kernels")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -433,6 +436,61 @@ def corun(chain, p50_alone, dev, steps=5, n=8192):
             "load_tflops_alone": round(load_alone, 1), "load_tflops_corun": round(load_busy, 1)}
 
 
+def time_whole_encoder(cfg, layers, dev, steps=2, warmup=1, img=224, patch=14, channels=3):
+    """Forward+backward of a whole ViT encoder on one micro-batch: patch
+    embedding of img x img images (no class token), `layers` sequential
+    layers (distinct weights) and a final LayerNorm, on this one GPU."""
+    from paper_2408_03505_amd import binding as B
+    import oracle
+    Bn, H = cfg["batch"], cfg["hidden"]
+    if (img // patch) ** 2 != cfg["seq"]:
+        return {"skipped": f"seq {cfg['seq']} is not ({img}/{patch})^2"}
+    K, kp = channels * patch * patch, B.patch_kp(channels, patch)
+    bf, f32 = dict(dtype=torch.bfloat16, device=dev), dict(dtype=torch.float32, device=dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    images = torch.randn(Bn, channels, img, img, **bf)
+    w_pe = torch.zeros(H, kp, **bf)
+    w_pe[:, :K].normal_(0, 0.02)
+    b_pe, pos = torch.empty(H, **bf).normal_(0, 0.02), torch.empty(cfg["seq"], H, **bf).normal_(0, 0.02)
+    shapes = B.param_shapes(cfg)
+    params = [{n: torch.empty(shapes[n], **bf).normal_(1.0 if n in ("ln1_g", "ln2_g") else 0.0, 0.02)
+               for n in B.PARAM_ORDER} for _ in range(layers)]
+    grads = [{n: torch.empty(shapes[n], **f32) for n in B.PARAM_ORDER} for _ in range(layers)]
+    lnf_g, lnf_b = torch.ones(H, **bf), torch.zeros(H, **bf)
+    lnf_grads = (torch.empty(H, **f32), torch.empty(H, **f32))
+    dout = torch.randn(Bn * cfg["seq"], H, **bf)
+    x0, patches = B.enc_patch_embed_fwd(images, patch, w_pe, b_pe, pos)
+    out, saved = B.encoder_stack_fwd(cfg, params, lnf_g, lnf_b, x0)
+    ws = torch.empty(B.stack_workspace_bytes(cfg, layers), dtype=torch.uint8, device=dev)
+    dx0 = torch.empty_like(x0)
+    pe_grads = B.enc_patch_embed_bwd(tuple(images.shape), patch, dout, patches, False)
+
+    def step():
+        B.enc_patch_embed_fwd(images, patch, w_pe, b_pe, pos, patches=patches, x0=x0)
+        B.encoder_stack_fwd(cfg, params, lnf_g, lnf_b, x0, out=out, saved=saved)
+        B.encoder_stack_bwd(cfg, params, lnf_g, x0, saved, dout, grads=grads, lnf_grads=lnf_grads, dx0=dx0, ws=ws)
+        B.enc_patch_embed_bwd(tuple(images.shape), patch, dx0, patches, False, grads=pe_grads)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    M = Bn * cfg["seq"]
+    flops = 3 * (layers * oracle.layer_flops(cfg) + 2 * M * H * K)
+    return {"layers": layers, "image": f"{img}x{img}, {patch}x{patch} patches, {channels} channels",
+            "ms_per_step": round(ms, 2), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "peak_memory_gb": round(torch.cuda.max_memory_allocated(dev) / 1e9, 1),
+            "note": "patch embedding + layers + final LayerNorm, forward and backward with fp32 gradients of "
+                    "every parameter, one micro-batch, all on this GPU"}
+
+
 class Chain:
     """Preallocated buffers and the kernel-by-kernel layer step."""
 
@@ -646,6 +704,12 @@ def main():
         res["corun"] = corun(chain, p50, dev)
     if not args.no_variants:
         res["variants"] = {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)}
+    if args.encoder_layers > 0:
+        try:
+            res["whole_encoder"] = time_whole_encoder(cfg, args.encoder_layers, dev)
+        except torch.cuda.OutOfMemoryError as e:
+            res["whole_encoder"] = {"error": f"out of memory: {str(e)[:200]}"}
+        torch.cuda.empty_cache()
     if not args.no_ceilings:
         ceil = measure_ceilings(dev)
         res["ceilings"] = ceil
