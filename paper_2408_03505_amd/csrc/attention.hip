@@ -152,6 +152,20 @@ __device__ __forceinline__ bf16x8_t tile_cols(const lds_char *t, int nbase, int 
   return lds_read_tr(t + tile_off(k, n >> 3) + in, t + tile_off(k + 4, n >> 3) + in);
 }
 
+// As tile_cols, but contraction index kk reads tile row 16st + perm23(kk):
+// the operand then meets registers whose tokens come in the order a
+// 32x32 MFMA result leaves them (bits 2 and 3 of the token index swapped),
+// so one natural-order tile serves both the row reads and this read.  The
+// transpose read takes each source lane's row address; lane half h (lanes
+// 32h..) supplies rows 4h + (lane % 16) / 4 for elements 0..3 and those
+// rows + 8 for elements 4..7.
+__device__ __forceinline__ bf16x8_t tile_cols_perm(const lds_char *t, int nbase, int st, int lane) {
+  const int k = st * 16 + 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int n = nbase + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int in = (n & 7) * 2;
+  return lds_read_tr(t + tile_off(k, n >> 3) + in, t + tile_off(k + 8, n >> 3) + in);
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
                                                        uint32_t qkv_bytes, bf16_t *__restrict__ o,
@@ -259,11 +273,10 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
 
 // ------------------------------------------------------------------ backward: dQ and D
 //
-// Per query tile: S^T = K Q^T and dP^T = V dO^T use K and V tiles stored with
-// permuted rows (perm23) and read by ds_read_b128, so the dS^T registers hold
-// keys in natural order per transpose-read position; dQ^T += K^T dS^T then
-// reads a second, natural-order copy of the K tile with ds_read_b64_tr_b16.
-// This kernel also writes D_i = dO_i . O_i for the dK/dV kernel.
+// Per query tile: S^T = K Q^T and dP^T = V dO^T read natural-order K and V
+// tiles with ds_read_b128; dQ^T += K^T dS^T reads the same K tile with the
+// permuted transpose read, which matches the token order of the dS^T
+// registers.  This kernel also writes D_i = dO_i . O_i for the dK/dV kernel.
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
@@ -272,7 +285,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
                                                               const bf16_t *__restrict__ dO, bf16_t *__restrict__ dqkv,
                                                               float *__restrict__ dvec) {
   using H = Head<D>;
-  constexpr int ROWS = 32 * NW, STAGE = 3 * kTileBytes;  // Kp, Vp, Kn
+  constexpr int ROWS = 32 * NW, STAGE = 2 * kTileBytes;  // K, V
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
   const lds_char *smem = (const lds_char *)(smem_raw);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
@@ -290,18 +303,16 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
   const size_t orow = (static_cast<size_t>(b) * S + q) * A + h * D;
 
   const u32x4_t rsrc = make_rsrc(qkv, qkv_bytes);
-  uint32_t voff_p[16 / NW], voff_n[16 / NW];
-  tile_voff<NW>(voff_p, wid, lane, ld, true);
-  tile_voff<NW>(voff_n, wid, lane, ld, false);
+  uint32_t voff[16 / NW];
+  tile_voff<NW>(voff, wid, lane, ld, false);
   const uint32_t k_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + A + h * D) * 2);
   const uint32_t v_base = k_base + static_cast<uint32_t>(A * 2);
   const uint32_t tile_step = static_cast<uint32_t>(kKT * ld * 2);
   auto issue = [&](int t) {
     const uint32_t buf = lds0 + (t & 1) * STAGE;
     const int rem = S - t * kKT;
-    tile_issue<NW>(rsrc, buf, voff_p, k_base + t * tile_step, wid, lane, rem, ld, true);
-    tile_issue<NW>(rsrc, buf + kTileBytes, voff_p, v_base + t * tile_step, wid, lane, rem, ld, true);
-    tile_issue<NW>(rsrc, buf + 2 * kTileBytes, voff_n, k_base + t * tile_step, wid, lane, rem, ld, false);
+    tile_issue<NW>(rsrc, buf, voff, k_base + t * tile_step, wid, lane, rem, ld, false);
+    tile_issue<NW>(rsrc, buf + kTileBytes, voff, v_base + t * tile_step, wid, lane, rem, ld, false);
   };
 
   bf16x8_t qf[H::KS], df[H::KS];
@@ -325,7 +336,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
   f32x16_t acc[H::NF];
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
-  constexpr int LOADS = 3 * (16 / NW);
+  constexpr int LOADS = 2 * (16 / NW);
   const int nk = (S + kKT - 1) / kKT;
   issue(0);
   for (int t = 0; t < nk; ++t) {
@@ -336,7 +347,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
       wait_vmcnt<0>();
     }
     block_barrier();
-    const lds_char *Kp = smem + (t & 1) * STAGE, *Vp = Kp + kTileBytes, *Kn = Kp + 2 * kTileBytes;
+    const lds_char *Ks = smem + (t & 1) * STAGE, *Vs = Ks + kTileBytes;
     const int k0 = t * kKT;
     f32x16_t sv[2], dp[2];
 #pragma unroll
@@ -345,23 +356,23 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
       dp[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) {
-        sv[f] = mfma32(tile_rows(Kp, f * 32, kk, lane), qf[kk], sv[f]);
-        dp[f] = mfma32(tile_rows(Vp, f * 32, kk, lane), df[kk], dp[f]);
+        sv[f] = mfma32(tile_rows(Ks, f * 32, kk, lane), qf[kk], sv[f]);
+        dp[f] = mfma32(tile_rows(Vs, f * 32, kk, lane), df[kk], dp[f]);
       }
     }
-    // register i of fragment f is key k0 + perm23(f*32 + 8(i/4) + 4 hf + i%4)
+    // register i of fragment f is key k0 + f*32 + 8(i/4) + 4 hf + i%4
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int key = k0 + perm23(f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3));
+        const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
         sv[f][i] = (key < S) ? exp2f(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
       }
 #pragma unroll
     for (int st = 0; st < kKT / 16; ++st) {
       const bf16x8_t sb = pack8(sv[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Kn, nf * 32, st, lane), sb, acc[nf]);
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Ks, nf * 32, st, lane), sb, acc[nf]);
     }
     block_barrier();
   }
@@ -372,10 +383,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
 
 // ------------------------------------------------------------------ backward: dK, dV
 //
-// Per key tile: S = Q K^T and dP = dO V^T use Q and dO tiles with permuted
-// rows (ds_read_b128); dV^T += dO^T P and dK^T += Q^T dS read natural-order
-// copies of dO and Q with ds_read_b64_tr_b16.  lse and D of the tile's
-// queries come in by DMA as well; queries past the sequence are masked out.
+// Per key tile: S = Q K^T and dP = dO V^T read natural-order Q and dO tiles
+// with ds_read_b128; dV^T += dO^T P and dK^T += Q^T dS read the same tiles
+// with the permuted transpose read.  lse and D of the tile's queries come in
+// by DMA as well; queries past the sequence are masked out.
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, int heads,
@@ -385,7 +396,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
                                                                 const float *__restrict__ dvec,
                                                                 bf16_t *__restrict__ dqkv) {
   using H = Head<D>;
-  constexpr int ROWS = 32 * NW, TILES = 4 * kTileBytes;  // Qp, dOp, Qn, dOn
+  constexpr int ROWS = 32 * NW, TILES = 2 * kTileBytes;  // Q, dO
   constexpr int STAGE = TILES + 2 * kKT * 4;             // + lse, D
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
   const lds_char *smem = (const lds_char *)(smem_raw);
@@ -403,11 +414,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
 
   const u32x4_t rq = make_rsrc(qkv, qkv_bytes), rd = make_rsrc(dO, do_bytes);
-  uint32_t vq_p[16 / NW], vq_n[16 / NW], vd_p[16 / NW], vd_n[16 / NW];
-  tile_voff<NW>(vq_p, wid, lane, ld, true);
-  tile_voff<NW>(vq_n, wid, lane, ld, false);
-  tile_voff<NW>(vd_p, wid, lane, A, true);
-  tile_voff<NW>(vd_n, wid, lane, A, false);
+  uint32_t vq[16 / NW], vd[16 / NW];
+  tile_voff<NW>(vq, wid, lane, ld, false);
+  tile_voff<NW>(vd, wid, lane, A, false);
   const uint32_t q_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + h * D) * 2);
   const uint32_t d_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * A + h * D) * 2);
   const uint32_t q_step = static_cast<uint32_t>(kKT * ld * 2), d_step = static_cast<uint32_t>(kKT * A * 2);
@@ -416,10 +425,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
   auto issue = [&](int t) {
     const uint32_t buf = lds0 + (t & 1) * STAGE;
     const int rem = S - t * kKT;
-    tile_issue<NW>(rq, buf, vq_p, q_base + t * q_step, wid, lane, rem, ld, true);
-    tile_issue<NW>(rd, buf + kTileBytes, vd_p, d_base + t * d_step, wid, lane, rem, A, true);
-    tile_issue<NW>(rq, buf + 2 * kTileBytes, vq_n, q_base + t * q_step, wid, lane, rem, ld, false);
-    tile_issue<NW>(rd, buf + 3 * kTileBytes, vd_n, d_base + t * d_step, wid, lane, rem, A, false);
+    tile_issue<NW>(rq, buf, vq, q_base + t * q_step, wid, lane, rem, ld, false);
+    tile_issue<NW>(rd, buf + kTileBytes, vd, d_base + t * d_step, wid, lane, rem, A, false);
     // lse (wave 0) and D (wave 1) of the tile's 64 queries; entries past the
     // sequence are masked out of P below
     const uint32_t vs = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((bh * S + t * kKT) * 4));
@@ -435,7 +442,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) dk[i] = dv[i] = f32x16_t{};
   const float c = kLog2e / sqrtf(static_cast<float>(D));
-  constexpr int LOADS = 4 * (16 / NW);
+  constexpr int LOADS = 2 * (16 / NW);
   const int nq = (S + kKT - 1) / kKT;
   issue(0);
   for (int t = 0; t < nq; ++t) {
@@ -449,8 +456,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
       wait_vmcnt<0>();
     }
     block_barrier();
-    const lds_char *Qp = smem + (t & 1) * STAGE, *Dp = Qp + kTileBytes;
-    const lds_char *Qn = Qp + 2 * kTileBytes, *Dn = Qp + 3 * kTileBytes;
+    const lds_char *Qs = smem + (t & 1) * STAGE, *Ds = Qs + kTileBytes;
     const float *Ls = reinterpret_cast<const float *>(smem_raw + (t & 1) * STAGE + TILES);
     const int q0 = t * kKT;
     f32x16_t sv[2], dp[2];
@@ -460,17 +466,16 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
       dp[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) {
-        sv[f] = mfma32(tile_rows(Qp, f * 32, kk, lane), kf[kk], sv[f]);
-        dp[f] = mfma32(tile_rows(Dp, f * 32, kk, lane), vf[kk], dp[f]);
+        sv[f] = mfma32(tile_rows(Qs, f * 32, kk, lane), kf[kk], sv[f]);
+        dp[f] = mfma32(tile_rows(Ds, f * 32, kk, lane), vf[kk], dp[f]);
       }
     }
-    // register 4g+e of fragment f is query perm23(f*32 + 8g + 4hf + e)
-    //   = f*32 + 16(g/2) + 8hf + 4(g%2) + e  (four consecutive queries)
+    // register 4g+e of fragment f is query f*32 + 8g + 4hf + e (four consecutive queries)
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int qi = f * 32 + 16 * (g >> 1) + 8 * hf + 4 * (g & 1);
+        const int qi = f * 32 + 8 * g + 4 * hf;
         const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi) * kLog2e;
         const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + kKT + qi);
 #pragma unroll
@@ -487,8 +492,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
       const bf16x8_t sb = pack8(dp[st >> 1], st & 1);
 #pragma unroll
       for (int nf = 0; nf < H::NF; ++nf) {
-        dv[nf] = mfma32(tile_cols(Dn, nf * 32, st, lane), pb, dv[nf]);
-        dk[nf] = mfma32(tile_cols(Qn, nf * 32, st, lane), sb, dk[nf]);
+        dv[nf] = mfma32(tile_cols_perm(Ds, nf * 32, st, lane), pb, dv[nf]);
+        dk[nf] = mfma32(tile_cols_perm(Qs, nf * 32, st, lane), sb, dk[nf]);
       }
     }
     block_barrier();  // every wave is done with this buffer before it is refilled
@@ -515,7 +520,7 @@ void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, c
   const uint32_t do_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * heads * D * 2);
   const int qblocks = B * heads * ((S + 32 * NWQ - 1) / (32 * NWQ));
   const int kblocks = B * heads * ((S + 32 * NWK - 1) / (32 * NWK));
-  constexpr int kDqLds = 2 * 3 * kTileBytes, kDkvLds = 2 * (4 * kTileBytes + 2 * kKT * 4);
+  constexpr int kDqLds = 2 * 2 * kTileBytes, kDkvLds = 2 * (2 * kTileBytes + 2 * kKT * 4);
   static const bool attrs_set = [] {
     hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dq_kernel<D, NWQ>),
                         hipFuncAttributeMaxDynamicSharedMemorySize, kDqLds);
