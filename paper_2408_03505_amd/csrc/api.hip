@@ -238,6 +238,9 @@ int attn_dims(const char *fn, int B, int S, int heads, int d) {
   if (d != 64 && d != 80 && d != 128) return fail(ENC_ERR_UNSUPPORTED, "%s: head_dim must be 64, 80 or 128", fn);
   if (static_cast<long>(B) * S * 3 * heads * d >= kMaxElems)
     return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  // the attention kernels address qkv (plus one tile of overhang) with 32-bit byte offsets
+  if ((static_cast<uint64_t>(B) * S + 64) * 3 * heads * d * 2 + 256 >= (1ull << 32))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: qkv exceeds the 4 GiB the attention kernels address", fn);
   return ENC_OK;
 }
 

@@ -355,3 +355,24 @@ def test_calibration_kernels():
     assert torch.equal(dst.view(torch.uint8), src)
     assert guard_intact(buf, dst.numel())
     assert torch.isfinite(out).all() and (out > 0).all()
+
+
+# --------------------------------------------------------------------------- maximum sizes
+
+def test_mlp_down_fwd_at_the_largest_accepted_operand():
+    """g holds 2^31 - 8192 elements (4 GiB - 16 KiB), past the 32-bit byte
+    offsets of the direct-to-LDS path: the register-staged kernel (64-bit
+    row offsets) takes it.  Sampled rows against the oracle."""
+    M, F, H = 87381, 24576, 64
+    announce(f"mlp_down_fwd largest operand M={M} F={F} H={H}")
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    g = torch.randn((M, F), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    w2 = cuda(random_bf16((H, F), 8, 0.02))
+    b2 = cuda(random_bf16((H,), 9, 0.02))
+    resid = cuda(random_bf16((M, H), 10))
+    out = B.enc_mlp_down_fwd(g, w2, b2, resid)
+    torch.cuda.synchronize()
+    rows = torch.tensor([0, 1, 40000, 87379, M - 1], device="cuda")
+    ref = oracle.linear_fwd(f64(g[rows]), f64(w2), f64(b2), resid=f64(resid[rows]))
+    assert max_rel(f64(out[rows]), ref) < TOL_ACT
+    del g

@@ -146,6 +146,11 @@ def test_bad_shapes_are_rejected():
     assert _status("enc_ln_fwd", 0, 64, p, p, p, ctypes.c_float(1e-6), p, p, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_ln_fwd", 4, 64, p, p, p, ctypes.c_float(-1.0), p, p, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_attn_fwd", 1, 8, 1, 96, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    # qkv just under 2^31 elements but past the attention kernels' 32-bit byte offsets
+    assert _status("enc_attn_fwd", 1, 116500, 48, 128, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert b"4 GiB" in B.lib().enc_last_error()
+    # per-kernel GEMM operands at 2^31 elements are refused
+    assert _status("enc_mlp_down_fwd", 87382, 24576, 64, p, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
     assert _status("enc_qkv_fwd", 8, 60, 64, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
     assert _status("enc_mlp_up_fwd", -1, 64, 64, p, p, p, p, p, s) == B.ENC_ERR_INVALID
 
