@@ -688,33 +688,43 @@ def main():
                      "traffic": read_traffic(dom) if args.config == "vit22b" else None,
                      "avg_launch_us": round(avg[dom], 2)},
     }
-    fit = {"trace": "synthetic LLM timeline: TP bubbles uniform in [200, 400] us alternating with "
-                    "LLM computation uniform in [300, 900] us (seed 0); kernels = per-kernel p50",
-           args.config: bubble_fit(p50)}
-    if args.fit_config and args.fit_config != args.config:
-        fcfg = CONFIGS[args.fit_config]
-        fx, fp, fd = layer_inputs(fcfg, seed=args.seed)
-        fchain = Chain(fcfg, fx.to(dev), {n: fp[n].to(dev) for n in fp}, fd.to(dev))
-        fp50 = time_chain(fchain, steps=10, warmup=3)
-        fit[args.fit_config] = bubble_fit(fp50)
-        fit[args.fit_config]["p50_us"] = {n: round(v, 2) for n, v in fp50.items()}
-        del fchain
-    res["bubble_fit"] = fit
-    if not args.no_corun:
-        res["corun"] = corun(chain, p50, dev)
-    if not args.no_variants:
-        res["variants"] = {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)}
-    if args.encoder_layers > 0:
+    def section(fn):
+        """Run an optional part of the report; a failure is recorded, not raised,
+        so that the measurement line above always gets printed."""
         try:
-            res["whole_encoder"] = time_whole_encoder(cfg, args.encoder_layers, dev)
-        except torch.cuda.OutOfMemoryError as e:
-            res["whole_encoder"] = {"error": f"out of memory: {str(e)[:200]}"}
-        torch.cuda.empty_cache()
+            return fn()
+        except Exception as e:  # noqa: BLE001
+            torch.cuda.synchronize()
+            return {"error": f"{type(e).__name__}: {str(e)[:300]}"}
+        finally:
+            torch.cuda.empty_cache()
+
+    def fit_report():
+        fit = {"trace": "synthetic LLM timeline: TP bubbles uniform in [200, 400] us alternating with "
+                        "LLM computation uniform in [300, 900] us (seed 0); kernels = per-kernel p50",
+               args.config: bubble_fit(p50)}
+        if args.fit_config and args.fit_config != args.config:
+            fcfg = CONFIGS[args.fit_config]
+            fx, fp, fd = layer_inputs(fcfg, seed=args.seed)
+            fchain = Chain(fcfg, fx.to(dev), {n: fp[n].to(dev) for n in fp}, fd.to(dev))
+            fp50 = time_chain(fchain, steps=10, warmup=3)
+            fit[args.fit_config] = bubble_fit(fp50)
+            fit[args.fit_config]["p50_us"] = {n: round(v, 2) for n, v in fp50.items()}
+        return fit
+
+    res["bubble_fit"] = section(fit_report)
+    if not args.no_corun:
+        res["corun"] = section(lambda: corun(chain, p50, dev))
+    if not args.no_variants:
+        res["variants"] = section(lambda: {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)})
+    if args.encoder_layers > 0:
+        res["whole_encoder"] = section(lambda: time_whole_encoder(cfg, args.encoder_layers, dev))
     if not args.no_ceilings:
-        ceil = measure_ceilings(dev)
+        ceil = section(lambda: measure_ceilings(dev))
         res["ceilings"] = ceil
-        res["roofline"]["measured_peak"] = ceil["mfma_bf16_tflops"]
-        res["roofline"]["frac_of_measured"] = round(achieved / ceil["mfma_bf16_tflops"], 4)
+        if "mfma_bf16_tflops" in ceil:
+            res["roofline"]["measured_peak"] = ceil["mfma_bf16_tflops"]
+            res["roofline"]["frac_of_measured"] = round(achieved / ceil["mfma_bf16_tflops"], 4)
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)

@@ -521,14 +521,6 @@ void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, c
   const int qblocks = B * heads * ((S + 32 * NWQ - 1) / (32 * NWQ));
   const int kblocks = B * heads * ((S + 32 * NWK - 1) / (32 * NWK));
   constexpr int kDqLds = 2 * 2 * kTileBytes, kDkvLds = 2 * (2 * kTileBytes + 2 * kKT * 4);
-  static const bool attrs_set = [] {
-    hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dq_kernel<D, NWQ>),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, kDqLds);
-    hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D, NWK>),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, kDkvLds);
-    return true;
-  }();
-  (void)attrs_set;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NWQ>), dim3(qblocks), dim3(NWQ * 64), kDqLds, s, B, S, heads,
                      qkv, qkv_bytes, o, lse, dO, dqkv, dvec);
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NWK>), dim3(kblocks), dim3(NWK * 64), kDkvLds, s, B, S, heads, qkv,
