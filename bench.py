@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--fit-config", default="vit22b_tp8",
                     help="a second workload whose chain is timed briefly and packed into the synthetic "
-                         "TP-bubble trace beside the main one ('' to skip)")
+                         "TP-bubble trace beside the main one ('' or 'none' to skip)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing the ViT-22B-style parallel block at the same shape")
     ap.add_argument("--no-corun", action="store_true",
@@ -703,7 +703,7 @@ def main():
         fit = {"trace": "synthetic LLM timeline: TP bubbles uniform in [200, 400] us alternating with "
                         "LLM computation uniform in [300, 900] us (seed 0); kernels = per-kernel p50",
                args.config: bubble_fit(p50)}
-        if args.fit_config and args.fit_config != args.config:
+        if args.fit_config not in ("", "none", args.config):
             fcfg = CONFIGS[args.fit_config]
             fx, fp, fd = layer_inputs(fcfg, seed=args.seed)
             fchain = Chain(fcfg, fx.to(dev), {n: fp[n].to(dev) for n in fp}, fd.to(dev))
