@@ -64,7 +64,7 @@ def parse():
 # GPU kernels of each chain entry, in launch order (a substring of each
 # dispatch's kernel name; every library kernel lives in namespace optimus)
 _GEMM = ("gemm_",)
-_LN_BWD = ("ln_bwd_dx_kernel", "ln_bwd_param_kernel", "ln_bwd_reduce_kernel")
+_LN_BWD = ("ln_bwd_kernel", "ln_bwd_reduce_kernel")
 ENTRY_KERNELS = {"ln1_fwd": ("ln_fwd_kernel",), "qkv_fwd": _GEMM, "attn_fwd": ("attn_fwd_kernel",),
                  "oproj_fwd": _GEMM, "ln2_fwd": ("ln_fwd_kernel",), "mlp_up_fwd": _GEMM, "mlp_down_fwd": _GEMM,
                  "mlp_down_bwd_data": _GEMM, "mlp_down_bwd_weight": _GEMM, "mlp_up_bwd_data": _GEMM,

@@ -43,6 +43,15 @@ __device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Workgroup barrier for hand-overs through LDS: waits for this wave's LDS
+// (and scalar) accesses only.  __syncthreads() also drains every outstanding
+// global load, which would stall loads issued ahead for later work.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Sum / max over the 64 lanes of a wave (butterfly; every lane gets the result).
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -6,10 +6,9 @@
 // reductions per row (a wave butterfly, plus an LDS exchange across the four
 // waves when TPR = 256).
 //
-// The backward is three kernels: dx (row-parallel, like the forward), the
-// column partial sums of dy * xhat and dy over row chunks (column-tiled with
-// 16-byte loads), and a fixed-order sum of those partials, so dgamma and
-// dbeta are deterministic.
+// The backward is two kernels: one pass over the rows that writes dx and
+// per-block column sums of dy * xhat and dy, and a fixed-order sum of those
+// partials, so dgamma and dbeta are deterministic.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -106,148 +105,281 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(int rows, int cols, co
   }
 }
 
-// dx = dresid + rstd * (ghat - mean(ghat) - xhat * mean(ghat * xhat)), ghat = dy * gamma
-template <int TPR, int CPT>
-__global__ __launch_bounds__(kThreads) void ln_bwd_dx_kernel(int rows, int cols, const bf16_t *__restrict__ dy,
-                                                             const bf16_t *__restrict__ x,
-                                                             const float *__restrict__ mean,
-                                                             const float *__restrict__ rstd,
-                                                             const bf16_t *__restrict__ gamma,
-                                                             const bf16_t *__restrict__ dresid,
-                                                             bf16_t *__restrict__ dx) {
-  __shared__ float red[4][2];
-  constexpr int RPB = kThreads / TPR;
-  const int t = threadIdx.x % TPR;
-  const int row = blockIdx.x * RPB + threadIdx.x / TPR;
-  if (row >= rows) return;
+// Backward, one pass over the rows.  Each block owns a contiguous range of
+// rows and walks it RG rows at a time (one row per TPR-thread group), with the
+// next row's loads in flight while the current row is reduced:
+//   dx = dresid + rstd * (ghat - mean(ghat) - xhat * mean(ghat * xhat)),
+//   ghat = dy * gamma.
+// Every thread keeps the column sums of dy * xhat and dy for its own columns
+// over the block's rows; the RG groups' sums are added in a fixed order
+// through LDS and the block writes one row of partials per gradient, which a
+// second kernel sums in a fixed order (deterministic dgamma / dbeta).
+// Blocks (partial rows) of the backward pass: one per CU.  Measured at
+// 2048 x 6144: 512, 1024 and 2048 blocks are slower (the partials grow with
+// the block count), and so is loading two rows ahead instead of one.
+constexpr int kBwdBlocks = 256;
+
+template <int TPR, int CPT, bool RES>
+__global__ __launch_bounds__(kThreads) void ln_bwd_kernel(int rows, int cols, int rows_per_block,
+                                                    const bf16_t *__restrict__ dy, const bf16_t *__restrict__ x,
+                                                    const float *__restrict__ mean, const float *__restrict__ rstd,
+                                                    const bf16_t *__restrict__ gamma,
+                                                    const bf16_t *__restrict__ dresid, bf16_t *__restrict__ dx,
+                                                    float *__restrict__ part) {
+  constexpr int RG = kThreads / TPR;  // row groups: rows in flight per block
+  __shared__ float red[kThreads / 64][2];
+  extern __shared__ __attribute__((aligned(16))) float comb[];  // [2][cols]
+  const int t = threadIdx.x % TPR, g = threadIdx.x / TPR;
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nch = cols >> 3;
-  const size_t off = static_cast<size_t>(row) * cols;
-  const float mu = mean[row], r = rstd[row];
-  float xh[CPT][8], gh[CPT][8];
-  float s[2] = {0.f, 0.f};
+  const int r_begin = blockIdx.x * rows_per_block;
+  const int r_end = min(rows, r_begin + rows_per_block);
+  // every group runs the same number of iterations (the block-wide barriers
+  // of TPR = 256 are reached by all threads); rows past r_end are masked
+  const int iters = (r_end - r_begin + RG - 1) / RG;
+
+  // This thread's chunks: idx[c] is clamped into the row so that every load
+  // is unconditional (the compiler can then count loads in flight exactly and
+  // wait for the current row only); chunks past the row end are masked at use.
+  int idx[CPT];
+  unsigned in_row = 0;
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
-    const int idx = t + TPR * c;
-    if (idx < nch) {
-      float d[8], xv[8], g[8];
-      unpack8(ldg16(dy + off + idx * 8), d);
-      unpack8(ldg16(x + off + idx * 8), xv);
-      unpack8(ldg16(gamma + idx * 8), g);
+    const int i = t + TPR * c;
+    idx[c] = min(i, nch - 1);
+    if (i < nch) in_row |= 1u << c;
+  }
+
+  float gm[CPT][8], sg[CPT][8], sb[CPT][8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        xh[c][e] = (xv[e] - mu) * r;
-        gh[c][e] = d[e] * g[e];
-        s[0] += gh[c][e];
-        s[1] += gh[c][e] * xh[c][e];
-      }
-    } else {
+  for (int c = 0; c < CPT; ++c) {
+    unpack8(ldg16(gamma + idx[c] * 8), gm[c]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) xh[c][e] = gh[c][e] = 0.f;
+    for (int e = 0; e < 8; ++e) {
+      if (!((in_row >> c) & 1u)) gm[c][e] = 0.f;
+      sg[c][e] = sb[c][e] = 0.f;
     }
   }
-  row_sum<TPR, 2>(s, &red);
+
+  // Row r's data and statistics (a row past r_end reads row r_end - 1, and
+  // its statistics are zeroed at use).  The statistics come with the row:
+  // loads retire in issue order, so loading them later would also wait for
+  // the row loaded ahead.
+  auto load = [&](int r, u32x4_t(&d)[CPT], u32x4_t(&xv)[CPT], u32x4_t(&res)[CPT], float &mu, float &rs) {
+    const int rr = min(r, r_end - 1);
+    const size_t off = static_cast<size_t>(rr) * cols;
+    mu = mean[rr];
+    rs = rstd[rr];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      d[c] = ldg16(dy + off + idx[c] * 8);
+      xv[c] = ldg16(x + off + idx[c] * 8);
+      if constexpr (RES) res[c] = ldg16(dresid + off + idx[c] * 8);
+    }
+  };
+  // sum over the TPR threads of this group (wave butterfly, then LDS across
+  // the group's four waves when TPR = 256)
+  auto group_sum = [&](float (&v)[2]) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) v[k] = wave_sum(v[k]);
+    if constexpr (TPR == 256) {
+      if (lane == 0) {
+        red[wid][0] = v[0];
+        red[wid][1] = v[1];
+      }
+      lds_barrier();  // the next row's loads stay in flight
+      const int w0 = g * 4;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) v[k] = ((red[w0][k] + red[w0 + 1][k]) + red[w0 + 2][k]) + red[w0 + 3][k];
+      lds_barrier();
+    }
+  };
+
   const float inv_n = 1.0f / static_cast<float>(cols);
-  const float c1 = s[0] * inv_n, c2 = s[1] * inv_n;
+  // One row: column sums, the row reduction, dx.  Rows past r_end are masked.
+  auto row = [&](int r, const u32x4_t(&cd)[CPT], const u32x4_t(&cx)[CPT], const u32x4_t(&cr)[CPT], float mu,
+                 float rs) {
+    const bool live = r < r_end;
+    const unsigned mask = live ? in_row : 0u;
+    if (!live) mu = rs = 0.f;
+    float s[2] = {0.f, 0.f};
 #pragma unroll
-  for (int c = 0; c < CPT; ++c) {
-    const int idx = t + TPR * c;
-    if (idx < nch) {
-      float res[8];
-      if (dresid)
-        unpack8(ldg16(dresid + off + idx * 8), res);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) res[e] = 0.f;
-      u32x4_t o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        o[e] = pack2(res[2 * e] + r * (gh[c][2 * e] - c1 - xh[c][2 * e] * c2),
-                     res[2 * e + 1] + r * (gh[c][2 * e + 1] - c1 - xh[c][2 * e + 1] * c2));
-      stg16(dx + off + idx * 8, o);
-    }
-  }
-}
-
-// Column partial sums over one chunk of rows: part[0][chunk][col] = sum dy * xhat,
-// part[1][chunk][col] = sum dy.  Block = 64 columns (8 chunks of 8) x 32 row
-// groups; the 32 group sums are added in a fixed order through LDS.
-constexpr int kParamCols = 64, kParamGroups = 32;
-
-__global__ __launch_bounds__(kThreads) void ln_bwd_param_kernel(int rows, int cols, int rows_per_chunk,
-                                                                const bf16_t *__restrict__ dy,
-                                                                const bf16_t *__restrict__ x,
-                                                                const float *__restrict__ mean,
-                                                                const float *__restrict__ rstd,
-                                                                float *__restrict__ part) {
-  __shared__ float red[2][kParamGroups][kParamCols + 1];
-  const int chunk = threadIdx.x & 7, grp = threadIdx.x >> 3;
-  const int c0 = blockIdx.x * kParamCols + chunk * 8;
-  const int r_begin = blockIdx.y * rows_per_chunk;
-  const int r_end = min(rows, r_begin + rows_per_chunk);
-  float sg[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, sb[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (c0 < cols) {
-#pragma unroll 2
-    for (int r = r_begin + grp; r < r_end; r += kParamGroups) {
-      const size_t off = static_cast<size_t>(r) * cols + c0;
+    for (int c = 0; c < CPT; ++c) {
       float d[8], xv[8];
-      unpack8(ldg16(dy + off), d);
-      unpack8(ldg16(x + off), xv);
-      const float mu = mean[r], rs = rstd[r];
+      unpack8(cd[c], d);
+      unpack8(cx[c], xv);
+      const bool in = (mask >> c) & 1u;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        sg[e] += d[e] * ((xv[e] - mu) * rs);
-        sb[e] += d[e];
+        // masked chunks contribute dy = 0: they add nothing
+        const float dv = in ? d[e] : 0.f;
+        const float xh = (xv[e] - mu) * rs, gh = dv * gm[c][e];
+        s[0] += gh;
+        s[1] += gh * xh;
+        sg[c][e] += dv * xh;
+        sb[c][e] += dv;
+      }
+    }
+    group_sum(s);
+    const float c1 = s[0] * inv_n, c2 = s[1] * inv_n;
+    const size_t off = static_cast<size_t>(r) * cols;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      if ((mask >> c) & 1u) {
+        // xhat and ghat again from the row still in registers
+        float d[8], xv[8], res[8], o8[8];
+        unpack8(cd[c], d);
+        unpack8(cx[c], xv);
+        if constexpr (RES) {
+          unpack8(cr[c], res);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) res[e] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float xh = (xv[e] - mu) * rs, gh = d[e] * gm[c][e];
+          o8[e] = res[e] + rs * (gh - c1 - xh * c2);
+        }
+        u32x4_t o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = pack2(o8[2 * e], o8[2 * e + 1]);
+        stg16(dx + off + idx[c] * 8, o);
+      }
+    }
+  };
+
+  if constexpr (CPT <= 4) {
+    // Two register buffers in turn: each row's loads are issued one row ahead
+    // (no register copies between iterations, which would wait for them).
+    // Pairs of iterations; an odd last one runs on a masked row.
+    u32x4_t d0[CPT], x0[CPT], q0[CPT], d1[CPT], x1[CPT], q1[CPT];
+    float mu0, rs0, mu1, rs1;
+    load(r_begin + g, d0, x0, q0, mu0, rs0);
+    for (int it = 0; it < iters; it += 2) {
+      const int r = r_begin + g + it * RG;
+      load(r + RG, d1, x1, q1, mu1, rs1);
+      row(r, d0, x0, q0, mu0, rs0);
+      load(r + 2 * RG, d0, x0, q0, mu0, rs0);
+      row(r + RG, d1, x1, q1, mu1, rs1);
+    }
+  } else {
+    // wide rows: no room for a second row in registers
+    u32x4_t d0[CPT], x0[CPT], q0[CPT];
+    float mu0, rs0;
+    for (int it = 0; it < iters; ++it) {
+      const int r = r_begin + g + it * RG;
+      load(r, d0, x0, q0, mu0, rs0);
+      row(r, d0, x0, q0, mu0, rs0);
+    }
+  }
+
+  // groups 1..RG-1 hand their column sums to group 0, one at a time
+#pragma unroll 1
+  for (int h = 1; h < RG; ++h) {
+    __syncthreads();
+    if (g == h) {
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) {
+        if ((in_row >> c) & 1u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            comb[idx[c] * 8 + e] = sg[c][e];
+            comb[cols + idx[c] * 8 + e] = sb[c][e];
+          }
+      }
+    }
+    __syncthreads();
+    if (g == 0) {
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) {
+        if ((in_row >> c) & 1u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            sg[c][e] += comb[idx[c] * 8 + e];
+            sb[c][e] += comb[cols + idx[c] * 8 + e];
+          }
       }
     }
   }
+  if (g == 0) {
+    float *pg = part + static_cast<size_t>(blockIdx.x) * cols;
+    float *pb = part + (static_cast<size_t>(gridDim.x) + blockIdx.x) * cols;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    red[0][grp][chunk * 8 + e] = sg[e];
-    red[1][grp][chunk * 8 + e] = sb[e];
-  }
-  __syncthreads();
-  if (threadIdx.x < 2 * kParamCols) {
-    const int which = threadIdx.x / kParamCols, cl = threadIdx.x % kParamCols;
-    const int col = blockIdx.x * kParamCols + cl;
-    float tsum = 0.f;
-#pragma unroll 8
-    for (int g = 0; g < kParamGroups; ++g) tsum += red[which][g][cl];
-    if (col < cols) part[(static_cast<size_t>(which) * gridDim.y + blockIdx.y) * cols + col] = tsum;
+    for (int c = 0; c < CPT; ++c) {
+      if ((in_row >> c) & 1u) {
+        const int i8 = idx[c] * 8;
+        *reinterpret_cast<f32x4_t *>(pg + i8) = f32x4_t{sg[c][0], sg[c][1], sg[c][2], sg[c][3]};
+        *reinterpret_cast<f32x4_t *>(pg + i8 + 4) = f32x4_t{sg[c][4], sg[c][5], sg[c][6], sg[c][7]};
+        *reinterpret_cast<f32x4_t *>(pb + i8) = f32x4_t{sb[c][0], sb[c][1], sb[c][2], sb[c][3]};
+        *reinterpret_cast<f32x4_t *>(pb + i8 + 4) = f32x4_t{sb[c][4], sb[c][5], sb[c][6], sb[c][7]};
+      }
+    }
   }
 }
 
-// dgamma/dbeta (+)= fixed-order sum of the row-chunk partials.
-__global__ __launch_bounds__(kThreads) void ln_bwd_reduce_kernel(int nchunks, int cols, const float *__restrict__ part,
+// dgamma (blockIdx.y 0) or dbeta (1) (+)= the fixed-order sum of the nblk
+// partial rows.  Block = 64 columns (8 chunks of 8) x 32 groups of partial
+// rows; the 32 group sums are added in a fixed order through LDS.
+constexpr int kRedCols = 64, kRedGroups = 32;
+
+__global__ __launch_bounds__(kThreads) void ln_bwd_reduce_kernel(int nblk, int cols, const float *__restrict__ part,
                                                                  float *__restrict__ dgamma,
                                                                  float *__restrict__ dbeta, int accumulate) {
-  const int col = blockIdx.x * kThreads + threadIdx.x;
-  if (col >= cols) return;
-  float g = 0.f, b = 0.f;
-  for (int c = 0; c < nchunks; ++c) {
-    g += part[static_cast<size_t>(c) * cols + col];
-    b += part[(static_cast<size_t>(nchunks) + c) * cols + col];
+  __shared__ float red[kRedGroups][kRedCols + 1];
+  const int chunk = threadIdx.x & 7, grp = threadIdx.x >> 3;
+  const int c0 = blockIdx.x * kRedCols + chunk * 8;
+  const float *src = part + static_cast<size_t>(blockIdx.y) * nblk * cols;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (c0 < cols) {
+#pragma unroll 4
+    for (int b = grp; b < nblk; b += kRedGroups) {
+      const float *q = src + static_cast<size_t>(b) * cols + c0;
+      const f32x4_t a = *reinterpret_cast<const f32x4_t *>(q);
+      const f32x4_t c = *reinterpret_cast<const f32x4_t *>(q + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] += a[e];
+        v[4 + e] += c[e];
+      }
+    }
   }
-  if (accumulate) {
-    g += dgamma[col];
-    b += dbeta[col];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[grp][chunk * 8 + e] = v[e];
+  __syncthreads();
+  if (threadIdx.x < kRedCols) {
+    const int col = blockIdx.x * kRedCols + threadIdx.x;
+    float tsum = 0.f;
+#pragma unroll 8
+    for (int q = 0; q < kRedGroups; ++q) tsum += red[q][threadIdx.x];
+    if (col < cols) {
+      float *out = blockIdx.y == 0 ? dgamma : dbeta;
+      out[col] = accumulate ? out[col] + tsum : tsum;
+    }
   }
-  dgamma[col] = g;
-  dbeta[col] = b;
 }
 
-// Row chunks of the parameter-gradient pass: about four blocks per CU.
-int param_chunks(int rows, int cols) {
-  const int col_blocks = (cols + kParamCols - 1) / kParamCols;
-  int chunks = (1024 + col_blocks - 1) / col_blocks;
-  const int max_chunks = (rows + kParamGroups - 1) / kParamGroups;  // keep >= 32 rows per chunk
-  if (chunks > max_chunks) chunks = max_chunks;
-  return chunks < 1 ? 1 : chunks;
+// Threads per row of the backward pass: one wave up to 2048 columns (four
+// rows in flight per 256-thread block), the whole block beyond.
+int bwd_tpr(int cols) { return (cols >> 3) > 256 ? 256 : 64; }
+
+// Rows per block of the backward pass (a multiple of the rows in flight).
+int bwd_rows_per_block(int rows, int cols) {
+  const int rg = kThreads / bwd_tpr(cols);
+  int rpb = (rows + kBwdBlocks - 1) / kBwdBlocks;
+  rpb = (rpb + rg - 1) / rg * rg;
+  return rpb < rg ? rg : rpb;
+}
+
+int bwd_blocks(int rows, int cols) {
+  const int rpb = bwd_rows_per_block(rows, cols);
+  return (rows + rpb - 1) / rpb;
 }
 
 }  // namespace
 
 size_t ln_bwd_ws_bytes(int rows, int cols) {
-  return static_cast<size_t>(param_chunks(rows, cols)) * static_cast<size_t>(cols) * 2 * sizeof(float);
+  return static_cast<size_t>(bwd_blocks(rows, cols)) * static_cast<size_t>(cols) * 2 * sizeof(float);
 }
 
 #define OPT_LN_DISPATCH(KERNEL, ...)                                                                           \
@@ -284,12 +416,39 @@ bool launch_ln_fwd(int rows, int cols, const bf16_t *x, const bf16_t *gamma, con
 bool launch_ln_bwd(int rows, int cols, const bf16_t *dy, const bf16_t *x, const float *mean, const float *rstd,
                    const bf16_t *gamma, const bf16_t *dresid, bf16_t *dx, float *dgamma, float *dbeta,
                    int accumulate, float *part, hipStream_t s) {
-  OPT_LN_DISPATCH(ln_bwd_dx_kernel, rows, cols, dy, x, mean, rstd, gamma, dresid, dx);
-  const int chunks = param_chunks(rows, cols);
-  const int rpc = (rows + chunks - 1) / chunks;
-  hipLaunchKernelGGL(ln_bwd_param_kernel, dim3((cols + kParamCols - 1) / kParamCols, chunks), dim3(kThreads), 0, s,
-                     rows, cols, rpc, dy, x, mean, rstd, part);
-  hipLaunchKernelGGL(ln_bwd_reduce_kernel, dim3((cols + kThreads - 1) / kThreads), dim3(kThreads), 0, s, chunks, cols,
+  const int nch = cols >> 3;
+  const int tpr = bwd_tpr(cols);
+  const int rpb = bwd_rows_per_block(rows, cols);
+  const int nblk = (rows + rpb - 1) / rpb;
+  const dim3 grid(nblk);
+  // LDS for the hand-over of column sums between the row groups of a block
+  const size_t comb = tpr < kThreads ? static_cast<size_t>(cols) * 2 * sizeof(float) : 0;
+#define OPT_LN_BWD(T, C)                                                                                       \
+  do {                                                                                                          \
+    if (dresid)                                                                                                 \
+      hipLaunchKernelGGL((ln_bwd_kernel<T, C, true>), grid, dim3(kThreads), comb, s, rows, cols, rpb, dy, x,      \
+                         mean, rstd, gamma, dresid, dx, part);                                                  \
+    else                                                                                                        \
+      hipLaunchKernelGGL((ln_bwd_kernel<T, C, false>), grid, dim3(kThreads), comb, s, rows, cols, rpb, dy, x,     \
+                         mean, rstd, gamma, dresid, dx, part);                                                  \
+  } while (0)
+  if (tpr == 256) {
+    const int cpt = (nch + 255) / 256;
+    if (cpt <= 2) OPT_LN_BWD(256, 2);
+    else if (cpt <= 3) OPT_LN_BWD(256, 3);
+    else if (cpt <= 4) OPT_LN_BWD(256, 4);
+    else if (cpt <= 6) OPT_LN_BWD(256, 6);
+    else if (cpt <= 8) OPT_LN_BWD(256, 8);
+    else return false;
+  } else {
+    const int cpt = (nch + 63) / 64;
+    if (cpt <= 1) OPT_LN_BWD(64, 1);
+    else if (cpt <= 2) OPT_LN_BWD(64, 2);
+    else if (cpt <= 3) OPT_LN_BWD(64, 3);
+    else OPT_LN_BWD(64, 4);
+  }
+#undef OPT_LN_BWD
+  hipLaunchKernelGGL(ln_bwd_reduce_kernel, dim3((cols + kRedCols - 1) / kRedCols, 2), dim3(kThreads), 0, s, nblk, cols,
                      part, dgamma, dbeta, accumulate);
   return true;
 }

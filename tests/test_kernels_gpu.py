@@ -70,7 +70,11 @@ def test_ln_fwd(rows, cols):
     assert guard_intact(ybuf, rows * cols) and guard_intact(mbuf, rows) and guard_intact(rbuf, rows)
 
 
-@pytest.mark.parametrize("rows,cols", [(394, 192), (1000, 768), (300, 6144), (7, 1280), (260, 2048)])
+# widths cover one wave per row (1-4 chunks per thread), a block per row (3, 5
+# and 8 chunks: the last without the next row loaded ahead), a single row and
+# row counts that leave the last block short
+@pytest.mark.parametrize("rows,cols", [(394, 192), (1000, 768), (300, 6144), (7, 1280), (260, 2048), (70, 16384),
+                                       (33, 10240), (1, 8), (2049, 4104)])
 @pytest.mark.parametrize("with_resid", [True, False])
 def test_ln_bwd(rows, cols, with_resid):
     announce(f"ln_bwd rows={rows} cols={cols} resid={with_resid}")
