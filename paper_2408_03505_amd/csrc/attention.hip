@@ -56,18 +56,39 @@ __device__ __forceinline__ void load_row_operand(bf16x8_t (&f)[Head<D>::KS], con
     f[kk] = valid ? as_bf16x8(ldg16(src + kk * 16 + hf * 8)) : as_bf16x8(u32x4_t{0u, 0u, 0u, 0u});
 }
 
-// Store a d-major 32x32 fragment set (rows d, lane = token) scaled by s.
+// Store a d-major result through this wave's 8 KB LDS slot.  The lane of
+// token t holds d values in 8-byte runs, so direct stores would touch 32 rows
+// per instruction; here the runs go to LDS row t (256-byte rows, 16-byte
+// chunk c stored at c ^ (t % 16)), and each lane then writes whole 16-byte
+// row segments: a quarter-wave covers one row, four rows per instruction.
+// dst is the row of the wave's first token, ld the row stride (elements),
+// ntok the wave's tokens inside the sequence (the rest are not stored).
 template <int D>
-__device__ __forceinline__ void store_dmajor(bf16_t *dst, const f32x16_t (&acc)[Head<D>::NF], float s, int hf) {
+__device__ __forceinline__ void store_dmajor_lds(bf16_t *dst, size_t ld, const f32x16_t (&acc)[Head<D>::NF], float s,
+                                                 int lane, lds_char *slot, int ntok) {
+  const int t = lane & 31, hf = lane >> 5;
 #pragma unroll
   for (int nf = 0; nf < Head<D>::NF; ++nf) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int d0 = nf * 32 + q * 8 + hf * 4;
       if (d0 < D) {
-        *reinterpret_cast<u32x2_t *>(dst + d0) =
+        const int c = d0 >> 3;
+        *reinterpret_cast<__attribute__((address_space(3))) u32x2_t *>(slot + t * 256 + ((c ^ (t & 15)) << 4) +
+                                                                        hf * 8) =
             u32x2_t{pack2(acc[nf][4 * q] * s, acc[nf][4 * q + 1] * s), pack2(acc[nf][4 * q + 2] * s, acc[nf][4 * q + 3] * s)};
       }
+    }
+  }
+  // LDS accesses of one wave run in order: the reads below see the writes
+  const int j = lane & 15;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = i * 4 + (lane >> 4);
+    if (j * 8 < D && r < ntok) {
+      const u32x4_t v =
+          *reinterpret_cast<const __attribute__((address_space(3))) u32x4_t *>(slot + r * 256 + ((j ^ (r & 15)) << 4));
+      stg16(dst + r * ld + j * 8, v);
     }
   }
 }
@@ -167,7 +188,7 @@ __device__ __forceinline__ bf16x8_t tile_cols_perm(const lds_char *t, int nbase,
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
                                                        uint32_t qkv_bytes, bf16_t *__restrict__ o,
                                                        float *__restrict__ lse) {
   using H = Head<D>;
@@ -265,10 +286,11 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(int B, int S, int heads, 
   }
 
   const float lt = l + __shfl_xor(l, 32, kWave);
-  if (qvalid) {
-    store_dmajor<D>(o + (static_cast<size_t>(b) * S + q) * A + h * D, acc, 1.0f / lt, hf);
-    if (hf == 0) lse[static_cast<size_t>(bh) * S + q] = (m + log2f(lt)) / kLog2e;
-  }
+  if (qvalid && hf == 0) lse[static_cast<size_t>(bh) * S + q] = (m + log2f(lt)) / kLog2e;
+  // the K/V buffers are free after the loop's last barrier
+  const int q0 = qt * kRows + wid * 32;
+  store_dmajor_lds<D>(o + (static_cast<size_t>(b) * S + q0) * A + h * D, A, acc, 1.0f / lt, lane,
+                      const_cast<lds_char *>(smem) + wid * 8192, S - q0);
 }
 
 // ------------------------------------------------------------------ backward: dQ and D
@@ -376,9 +398,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
     }
     block_barrier();
   }
-  if (qvalid)
-    store_dmajor<D>(dqkv + (static_cast<size_t>(b) * S + q) * ld + h * D, acc, 1.0f / sqrtf(static_cast<float>(D)),
-                    hf);
+  const int q0 = qt * ROWS + wid * 32;
+  store_dmajor_lds<D>(dqkv + (static_cast<size_t>(b) * S + q0) * ld + h * D, ld, acc,
+                      1.0f / sqrtf(static_cast<float>(D)), lane, const_cast<lds_char *>(smem) + wid * 8192, S - q0);
 }
 
 // ------------------------------------------------------------------ backward: dK, dV
@@ -498,11 +520,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
     }
     block_barrier();  // every wave is done with this buffer before it is refilled
   }
-  if (kvalid) {
-    bf16_t *row = dqkv + (static_cast<size_t>(b) * S + key) * ld + h * D;
-    store_dmajor<D>(row + A, dk, 1.0f / sqrtf(static_cast<float>(D)), hf);
-    store_dmajor<D>(row + 2 * A, dv, 1.0f, hf);
-  }
+  const int k0w = kt * ROWS + wid * 32;
+  bf16_t *row = dqkv + (static_cast<size_t>(b) * S + k0w) * ld + h * D;
+  lds_char *slots = const_cast<lds_char *>(smem);
+  store_dmajor_lds<D>(row + A, ld, dk, 1.0f / sqrtf(static_cast<float>(D)), lane, slots + wid * 8192, S - k0w);
+  store_dmajor_lds<D>(row + 2 * A, ld, dv, 1.0f, lane, slots + (NW + wid) * 8192, S - k0w);
 }
 
 template <int D>
