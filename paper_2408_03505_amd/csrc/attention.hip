@@ -32,6 +32,12 @@ constexpr int kKT = 64;     // keys (forward, dQ) or queries (dK/dV) per LDS til
 constexpr int kRows = 128;  // queries (or keys) per workgroup: 4 waves x 32
 constexpr float kLog2e = 1.4426950408889634f;
 
+// 2^x on the hardware exponential (v_exp_f32).  Every argument here is a
+// logit minus a running maximum or the log-sum-exp, so x <= 0 up to rounding
+// and -inf for masked keys: results lie in [0, 1] and those below the fp32
+// normal range flush to zero, which only drops weights under 2^-126.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 template <int D>
 struct Head {
   static constexpr int KS = D / 16;              // 16-wide contraction steps over d
@@ -262,14 +268,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
         mt = fmaxf(mt, x);
       }
     mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
-    const float alpha = exp2f(m - mt);
+    const float alpha = exp2_hw(m - mt);
     m = mt;
     float ls = 0.f;
 #pragma unroll
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float pv = exp2f(s[f][i] - mt);
+        const float pv = exp2_hw(s[f][i] - mt);
         s[f][i] = pv;
         ls += pv;
       }
@@ -388,7 +394,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-        sv[f][i] = (key < S) ? exp2f(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
+        sv[f][i] = (key < S) ? exp2_hw(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
       }
 #pragma unroll
     for (int st = 0; st < kKT / 16; ++st) {
@@ -503,7 +509,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const bool ok = q0 + qi + e < S;
-          const float pv = exp2f(sv[f][4 * g + e] * c - l4[e]);
+          const float pv = exp2_hw(sv[f][4 * g + e] * c - l4[e]);
           sv[f][4 * g + e] = ok ? pv : 0.f;
           dp[f][4 * g + e] = ok ? pv * (dp[f][4 * g + e] - d4[e]) : 0.f;
         }
