@@ -23,8 +23,8 @@
 // gradient as row sums of the transposed A operand (deterministic).
 //
 // Workgroup order is XCD-aware: MI355X dispatches workgroup i to XCD i % 8,
-// so logical tile ids are remapped to give each XCD one contiguous range,
-// ordered M-fastest in groups, which keeps each weight slab in one XCD's L2.
+// so each XCD is given its own block of the tile grid, walked M-fastest in
+// groups of row tiles, which keeps the operand panels it shares in its L2.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "lds_dma.hpp"
@@ -41,11 +41,28 @@ __device__ __forceinline__ float gelu_grad_f(float u) {
   return Phi + u * phi;
 }
 
-// Logical tile id for this workgroup: contiguous per XCD, then grouped so
-// that GROUP_M row tiles sweep one column tile before moving on.
+// Logical tile for this workgroup.  MI355X dispatches workgroup i to XCD
+// i % 8.  When the tile grid splits evenly, the XCDs form two halves along
+// M, the four XCDs of a half split its column tiles, and each XCD walks its
+// block of tiles in groups of 4 row tiles that sweep the block's columns.
+// Otherwise each XCD takes one contiguous range of logical tiles, grouped by
+// 8 row tiles.  (Measured on the twelve ViT-22B layer GEMMs: 0.7% less time
+// in total than the contiguous order, from 5% on the MLP-up weight gradient
+// to -2% on the QKV weight gradient.)
 __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int &tm, int &tn) {
   const int pid = blockIdx.x, nb = gridDim.x;
   const int xcd = pid & 7, local = pid >> 3;
+  if (tiles_m % 2 == 0 && tiles_n % 4 == 0) {
+    constexpr int GM = 4;
+    const int rows_p = tiles_m / 2, cols_x = tiles_n / 4;
+    const int gs = GM * cols_x;
+    const int g = local / gs, first_m = g * GM;
+    const int gm = min(rows_p - first_m, GM);
+    const int in_g = local - g * gs;
+    tm = (xcd >> 2) * rows_p + first_m + in_g % gm;
+    tn = (xcd & 3) * cols_x + in_g / gm;
+    return;
+  }
   const int per = nb >> 3, rem = nb & 7;
   const int logical = (xcd < rem) ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
   constexpr int GROUP_M = 8;
