@@ -38,6 +38,17 @@ constexpr float kLog2e = 1.4426950408889634f;
 // normal range flush to zero, which only drops weights under 2^-126.
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Work item (sequence-head bh, tile sub) of this workgroup.  The nsub blocks
+// of one sequence-head read the same K/V (or Q/dO) tiles, so they are placed
+// on one XCD (workgroup i runs on XCD i % 8) to share its L2: each XCD takes
+// a contiguous range of items when the grid splits evenly over the 8 XCDs.
+__device__ __forceinline__ void block_item(int nsub, int &bh, int &sub) {
+  const int pid = blockIdx.x, nb = gridDim.x;
+  const int item = (nb & 7) ? pid : (pid & 7) * (nb >> 3) + (pid >> 3);
+  bh = item / nsub;
+  sub = item % nsub;
+}
+
 template <int D>
 struct Head {
   static constexpr int KS = D / 16;              // 16-wide contraction steps over d
@@ -203,8 +214,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
   const int nqt = (S + kRows - 1) / kRows;
-  const int qt = blockIdx.x % nqt;
-  const int bh = blockIdx.x / nqt;
+  int bh, qt;
+  block_item(nqt, bh, qt);
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
   const int lane = threadIdx.x & 63, hf = lane >> 5;
@@ -319,8 +330,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
   const int nqt = (S + ROWS - 1) / ROWS;
-  const int qt = blockIdx.x % nqt;
-  const int bh = blockIdx.x / nqt;
+  int bh, qt;
+  block_item(nqt, bh, qt);
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
   const int lane = threadIdx.x & 63, hf = lane >> 5;
@@ -431,8 +442,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
   const int nkt = (S + ROWS - 1) / ROWS;
-  const int kt = blockIdx.x % nkt;
-  const int bh = blockIdx.x / nkt;
+  int bh, kt;
+  block_item(nkt, bh, kt);
   const int b = bh / heads, h = bh % heads;
   const int A = heads * D, ld = 3 * A;
   const int lane = threadIdx.x & 63, hf = lane >> 5;
