@@ -48,6 +48,10 @@ def parse():
     ap.add_argument("--encoder-layers", type=int, default=48,
                     help="also time the whole encoder (patch embedding + this many layers + final LayerNorm) "
                          "at the workload's shape; 0 skips it")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip timing the layer chain at the other workloads (ViT-Tiny/Base/Huge, TP shard)")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="skip timing the memory-bound kernels after a 512 MiB cache flush")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-only and device-copy reference kernels")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -320,12 +324,64 @@ def time_chain(chain, steps, warmup):
             for i, n in enumerate(names)}
 
 
+MEM_BOUND = ("ln1_fwd", "ln2_fwd", "ln2_bwd", "ln1_bwd")
+
+
+def time_flushed(chain, work, reps=20, flush_mib=512):
+    """The memory-bound entries timed on their own: warm (launches back to
+    back) and cold (each launch after writing a 512 MiB buffer, which evicts
+    the 256 MB Infinity Cache and the L2s).  p50 of reps launches each."""
+    fns = dict(chain.kernels)
+    flush = torch.empty(flush_mib << 20, dtype=torch.uint8, device=chain.x.device)
+    out = {}
+    for n in MEM_BOUND:
+        fn = fns[n]
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        res = {}
+        for mode in ("warm", "flushed"):
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+            for i in range(reps):
+                if mode == "flushed":
+                    flush.fill_(i & 255)
+                ev[i][0].record()
+                fn()
+                ev[i][1].record()
+            torch.cuda.synchronize()
+            us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+            res[f"{mode}_p50_us"] = round(us, 2)
+            res[f"{mode}_gbs"] = round(work[n][1] / (us * 1e-6) / 1e9, 1)
+        out[n] = res
+    del flush
+    return out
+
+
+def time_configs(main, dev, seed, steps=10, warmup=3):
+    """The layer chain at every other workload: step time (sum of per-kernel
+    p50), rate, and the slowest kernel."""
+    from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs
+    out = {}
+    for name, cfg in CONFIGS.items():
+        if name == main:
+            continue
+        x, params, dout = layer_inputs(cfg, seed=seed)
+        ch = Chain(cfg, x.to(dev), {n: params[n].to(dev) for n in params}, dout.to(dev))
+        p50 = time_chain(ch, steps=steps, warmup=warmup)
+        ms = sum(p50.values()) / 1e3
+        worst = max(p50, key=p50.get)
+        out[name] = {"sum_kernel_p50_ms": round(ms, 4),
+                     "tflops": round(step_flops(cfg) / (ms * 1e-3) / 1e12, 1),
+                     "max_kernel_p50_us": round(p50[worst], 2), "max_kernel": worst}
+        del ch
+    return out
+
+
 def time_parallel_block(cfg, dev, steps=10, warmup=3):
     """Forward+backward of the ViT-22B-style parallel block (composite entry
     points) at the same shape, plus its two QK-norm kernels on their own."""
     from paper_2408_03505_amd import binding as B
     from paper_2408_03505_amd.synthetic import PPARAM_ORDER, parallel_block_inputs
-    import oracle
     x, p, d = parallel_block_inputs(cfg, seed=0)
     gx, gd = x.to(dev), d.to(dev)
     gp = {n: p[n].to(dev) for n in PPARAM_ORDER}
@@ -352,7 +408,7 @@ def time_parallel_block(cfg, dev, steps=10, warmup=3):
         step()
     torch.cuda.synchronize()
     ms = p50_ms(step, steps)
-    flops = 3 * oracle.layer_flops(cfg)
+    flops = step_flops(cfg)
     v = B.parallel_saved_views(cfg, saved)
     nh, dd, M = cfg["heads"], cfg["head_dim"], cfg["batch"] * cfg["seq"]
     qkvn, st = v["qkvn"].clone(), v["qkstats"].clone()
@@ -441,7 +497,6 @@ def time_whole_encoder(cfg, layers, dev, steps=2, warmup=1, img=224, patch=14, c
     embedding of img x img images (no class token), `layers` sequential
     layers (distinct weights) and a final LayerNorm, on this one GPU."""
     from paper_2408_03505_amd import binding as B
-    import oracle
     Bn, H = cfg["batch"], cfg["hidden"]
     if (img // patch) ** 2 != cfg["seq"]:
         return {"skipped": f"seq {cfg['seq']} is not ({img}/{patch})^2"}
@@ -482,7 +537,7 @@ def time_whole_encoder(cfg, layers, dev, steps=2, warmup=1, img=224, patch=14, c
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     M = Bn * cfg["seq"]
-    flops = 3 * (layers * oracle.layer_flops(cfg) + 2 * M * H * K)
+    flops = layers * step_flops(cfg) + 3 * 2 * M * H * K
     return {"layers": layers, "image": f"{img}x{img}, {patch}x{patch} patches, {channels} channels",
             "ms_per_step": round(ms, 2), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
             "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
@@ -571,6 +626,12 @@ def kernel_work(cfg):
     }
 
 
+def step_flops(cfg):
+    """Algorithmic flops of one layer forward + backward (three times the
+    forward: the backward has two products per forward product)."""
+    return sum(f for f, _ in kernel_work(cfg).values())
+
+
 def cpu_baseline(cfg, x, params, dout, budget_s):
     """The float64 oracle's layer forward+backward on whole sequences of the
     same workload (as many as fit the time budget, at least one)."""
@@ -624,7 +685,6 @@ def main():
                                    "(--gpus must be 1)"}), flush=True)
         sys.exit(2)
     from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs
-    import oracle
 
     cfg = CONFIGS[args.config]
     x, params, dout = layer_inputs(cfg, seed=args.seed)
@@ -677,15 +737,14 @@ def main():
     dom_us = [a.elapsed_time(b) * 1e3 for a, b in dev_ev]
 
     work = kernel_work(cfg)
-    flops_step = 3 * oracle.layer_flops(cfg)
-    assert abs(sum(w[0] for w in work.values()) - flops_step) < 1e-6 * flops_step
+    flops_step = step_flops(cfg)
     ms = wall / K * 1e3
     tflops = flops_step / (wall / K) / 1e12
     avg = {n: float(np.mean(v)) for n, v in per.items()}
     avg[dom] = float(np.mean(dom_us))
     dflops = work[dom][0]
     achieved = dflops / (avg[dom] * 1e-6) / 1e12
-    per_kernel = {n: {"p50_us": round(p50[n], 2),
+    per_kernel = {n: {"p50_us": round(p50[n], 2), "p90_us": round(float(np.percentile(per[n], 90)), 2),
                       "tflops": round(work[n][0] / (p50[n] * 1e-6) / 1e12, 1) if work[n][0] else None,
                       "gbs": round(work[n][1] / (p50[n] * 1e-6) / 1e9, 1),
                       "frac": round((work[n][0] / (p50[n] * 1e-6) / 1e12) / PEAK_BF16_TFLOPS, 3) if work[n][0]
@@ -738,6 +797,10 @@ def main():
         res["variants"] = section(lambda: {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)})
     if args.encoder_layers > 0:
         res["whole_encoder"] = section(lambda: time_whole_encoder(cfg, args.encoder_layers, dev))
+    if not args.no_flush:
+        res["memory_bound"] = section(lambda: time_flushed(chain, work))
+    if not args.no_configs:
+        res["configs"] = section(lambda: time_configs(args.config, dev, args.seed))
     if not args.no_ceilings:
         ceil = section(lambda: measure_ceilings(dev))
         res["ceilings"] = ceil

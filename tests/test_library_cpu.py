@@ -216,3 +216,13 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         B.lib()
+
+
+def test_bench_flop_count_matches_the_oracle():
+    # the bench counts flops from its own per-kernel table; it must agree with
+    # the oracle's count of one layer forward (times three for fwd + bwd)
+    import bench
+    import oracle
+    from paper_2408_03505_amd.synthetic import CONFIGS
+    for name, cfg in CONFIGS.items():
+        assert bench.step_flops(cfg) == 3 * oracle.layer_flops(cfg), name
