@@ -1,0 +1,124 @@
+"""Host-side logic of bench.py (no GPU): dispatch-to-entry mapping of a
+kernel trace, FETCH/WRITE scaling against the copy reference, the committed
+traffic table and its source hash, the bubble packing report, and the refusal
+of multi-GPU runs."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _one_step_names():
+    """Kernel names of one chain step, as a trace would show them."""
+    out = []
+    for entry, kernels in bench.ENTRY_KERNELS.items():
+        for k in kernels:
+            out.append(f"void optimus::(anonymous namespace)::{k}<256, 3>(int, int)")
+    return out
+
+
+def test_map_dispatches_sums_each_entry_per_step():
+    names = _one_step_names()
+    per_step = len(names)
+    lib = [(i, names[i % per_step], float(i)) for i in range(2 * per_step)]
+    steps = bench.map_dispatches(lib[::-1])  # order of the input does not matter
+    assert len(steps) == 2
+    i = 0
+    for n in bench.ENTRY_KERNELS:
+        d = bench.DISPATCHES[n]
+        for st in range(2):
+            want = sum(float(st * per_step + i + j) for j in range(d))
+            assert steps[st][n] == want, (n, st)
+        i += d
+
+
+def test_map_dispatches_rejects_partial_steps_and_wrong_kernels():
+    names = _one_step_names()
+    lib = [(i, names[i], 1.0) for i in range(len(names))]
+    with pytest.raises(RuntimeError, match="whole number"):
+        bench.map_dispatches(lib[:-1])
+    swapped = list(lib)
+    swapped[1], swapped[2] = (1, names[2], 1.0), (2, names[1], 1.0)  # qkv GEMM <-> attention
+    with pytest.raises(RuntimeError, match="is not"):
+        bench.map_dispatches(swapped)
+
+
+def _write_counters(d, counter, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "1_counter_collection.csv"), "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for i, (name, value) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i, "Kernel_Name": name, "Counter_Name": counter, "Counter_Value": value})
+
+
+def test_pmc_traffic_scales_by_the_copy_reference(tmp_path):
+    names = _one_step_names()
+    copy_bytes = 1 << 30
+    # the copy's FETCH_SIZE reads half its bytes (KiB), WRITE_SIZE all of them
+    fetch = [("__amd_rocclr_copyBuffer", copy_bytes / 2 / 1024)] + [(n, 100.0) for n in names]
+    write = [("__amd_rocclr_copyBuffer", copy_bytes / 1024)] + [(n, 10.0) for n in names]
+    _write_counters(str(tmp_path / "f"), "FETCH_SIZE", fetch)
+    _write_counters(str(tmp_path / "w"), "WRITE_SIZE", write)
+    vals = bench.pmc_traffic(str(tmp_path / "f"), str(tmp_path / "w"), copy_bytes)
+    f, fs = vals["FETCH_SIZE"]
+    w, ws = vals["WRITE_SIZE"]
+    assert fs == pytest.approx(2.0) and ws == pytest.approx(1.0)
+    for n in bench.ENTRY_KERNELS:
+        d = bench.DISPATCHES[n]
+        assert f[n] == pytest.approx(d * 100.0 * 1024 * 2.0)
+        assert w[n] == pytest.approx(d * 10.0 * 1024)
+
+
+def test_committed_traffic_table_is_keyed_by_the_sources():
+    # an entry has a traffic figure exactly when the committed table was taken
+    # on its family's current sources, and a changed source hash voids it
+    text = open(bench.TRAFFIC_MD).read()
+    for n in bench.ENTRY_KERNELS:
+        fam = bench.entry_family(n)
+        current = f"source-sha256 {fam}: {bench.source_hash(fam)}" in text
+        t = bench.read_traffic(n)
+        assert (t is not None and t > 0) if current else t is None, n
+    real = bench.source_hash
+    try:
+        bench.source_hash = lambda fam: "0" * 64
+        assert bench.read_traffic("qkv_fwd") is None
+    finally:
+        bench.source_hash = real
+
+
+def test_kernel_work_covers_every_entry():
+    from paper_2408_03505_amd.synthetic import CONFIGS
+    for cfg in CONFIGS.values():
+        work = bench.kernel_work(cfg)
+        assert set(work) == set(bench.ENTRY_KERNELS)
+        assert all(f >= 0 and b > 0 for f, b in work.values())
+        # memory-bound entries carry no flops; every other entry does
+        assert all((work[n][0] == 0) == (n in bench.MEM_BOUND) for n in work)
+
+
+def test_bubble_fit_packs_in_chain_order():
+    # a 150 us kernel fits any 200-400 us bubble; a 500 us kernel fits none
+    p50 = {n: 150.0 for n in bench.ENTRY_KERNELS}
+    r = bench.bubble_fit(p50)
+    assert r["fwd"]["placed"] == r["fwd"]["kernels"] and r["bwd"]["placed"] == r["bwd"]["kernels"]
+    assert 0 < r["fwd"]["fill"] <= 1 and 0 < r["bwd"]["fill"] <= 1
+    p50["qkv_fwd"] = 500.0
+    r = bench.bubble_fit(p50)
+    assert r["fwd"]["blocked_at"] == "qkv_fwd" and r["fwd"]["placed"] == 1
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 2
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in line["error"]
