@@ -422,21 +422,28 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
 
 // ------------------------------------------------------------------ backward: dK, dV
 //
-// Per key tile: S = Q K^T and dP = dO V^T read natural-order Q and dO tiles
-// with ds_read_b128; dV^T += dO^T P and dK^T += Q^T dS read the same tiles
-// with the permuted transpose read.  lse and D of the tile's queries come in
-// by DMA as well; queries past the sequence are masked out.
+// Per block of 32·NG keys, two waves share each group of 32 keys.  Wave A
+// (waves 0..NG-1) computes S = Q K^T, P = exp(S - lse) and dV^T += dO^T P;
+// wave B (waves NG..2NG-1) computes dP = dO V^T, dS = P ∘ (dP - D) and
+// dK^T += Q^T dS.  P goes from A to B through LDS in fp32, in the MFMA
+// result layout both waves hold (lane = key, registers = queries), so dS is
+// exactly what one wave computing both would get.  Each wave keeps one row
+// operand and one d-major accumulator, which fits two waves per SIMD.  The
+// Q and dO tiles are natural-order; S and dP read them with ds_read_b128,
+// the dV and dK products with the permuted transpose read.  lse and D of the
+// tile's queries come in by DMA; queries past the sequence are masked out.
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, int heads,
-                                                                const bf16_t *__restrict__ qkv, uint32_t qkv_bytes,
-                                                                const float *__restrict__ lse,
-                                                                const bf16_t *__restrict__ dO, uint32_t do_bytes,
-                                                                const float *__restrict__ dvec,
-                                                                bf16_t *__restrict__ dqkv) {
+template <int D, int NG>
+__global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, int heads,
+                                                                 const bf16_t *__restrict__ qkv, uint32_t qkv_bytes,
+                                                                 const float *__restrict__ lse,
+                                                                 const bf16_t *__restrict__ dO, uint32_t do_bytes,
+                                                                 const float *__restrict__ dvec,
+                                                                 bf16_t *__restrict__ dqkv) {
   using H = Head<D>;
-  constexpr int ROWS = 32 * NW, TILES = 2 * kTileBytes;  // Q, dO
-  constexpr int STAGE = TILES + 2 * kKT * 4;             // + lse, D
+  constexpr int NW = 2 * NG, ROWS = 32 * NG, TILES = 2 * kTileBytes;  // Q, dO
+  constexpr int STAGE = TILES + 2 * kKT * 4;                           // + lse, D
+  constexpr int PX = 2 * STAGE;  // P hand-over: one 8 KB slot per key group
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
   const lds_char *smem = (const lds_char *)(smem_raw);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
@@ -448,7 +455,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
   const int A = heads * D, ld = 3 * A;
   const int lane = threadIdx.x & 63, hf = lane >> 5;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int key = kt * ROWS + wid * 32 + (lane & 31);
+  const bool role_a = wid < NG;  // wave-uniform
+  const int grp = role_a ? wid : wid - NG;
+  const int k0w = kt * ROWS + grp * 32;
+  const int key = k0w + (lane & 31);
   const bool kvalid = key < S;
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
 
@@ -473,13 +483,14 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
     if (wid == 1) buffer_load_lds4(rv, __builtin_amdgcn_readfirstlane(buf + TILES + kKT * 4), lane * 4, vs);
   };
 
-  bf16x8_t kf[H::KS], vf[H::KS];
-  load_row_operand<D>(kf, base + static_cast<size_t>(key) * ld + A + h * D, kvalid, hf);
-  load_row_operand<D>(vf, base + static_cast<size_t>(key) * ld + 2 * A + h * D, kvalid, hf);
+  // K rows (wave A) or V rows (wave B) of this lane's key
+  bf16x8_t rf[H::KS];
+  load_row_operand<D>(rf, base + static_cast<size_t>(key) * ld + (role_a ? A : 2 * A) + h * D, kvalid, hf);
 
-  f32x16_t dk[H::NF], dv[H::NF];
+  f32x16_t acc[H::NF];  // dV^T (wave A) or dK^T (wave B)
 #pragma unroll
-  for (int i = 0; i < H::NF; ++i) dk[i] = dv[i] = f32x16_t{};
+  for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
+  float *px = reinterpret_cast<float *>(smem_raw + PX) + grp * (32 * 64);
   const float c = kLog2e / sqrtf(static_cast<float>(D));
   constexpr int LOADS = 2 * (16 / NW);
   const int nq = (S + kKT - 1) / kKT;
@@ -498,50 +509,60 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(int B, int S, in
     const lds_char *Qs = smem + (t & 1) * STAGE, *Ds = Qs + kTileBytes;
     const float *Ls = reinterpret_cast<const float *>(smem_raw + (t & 1) * STAGE + TILES);
     const int q0 = t * kKT;
-    f32x16_t sv[2], dp[2];
+    // S^T (wave A) or dP^T (wave B): register 4g+e of fragment f is query
+    // f*32 + 8g + 4hf + e (four consecutive queries)
+    const lds_char *Rs = role_a ? Qs : Ds;
+    f32x16_t sv[2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       sv[f] = f32x16_t{};
-      dp[f] = f32x16_t{};
 #pragma unroll
-      for (int kk = 0; kk < H::KS; ++kk) {
-        sv[f] = mfma32(tile_rows(Qs, f * 32, kk, lane), kf[kk], sv[f]);
-        dp[f] = mfma32(tile_rows(Ds, f * 32, kk, lane), vf[kk], dp[f]);
-      }
+      for (int kk = 0; kk < H::KS; ++kk) sv[f] = mfma32(tile_rows(Rs, f * 32, kk, lane), rf[kk], sv[f]);
     }
-    // register 4g+e of fragment f is query f*32 + 8g + 4hf + e (four consecutive queries)
+    if (role_a) {
 #pragma unroll
-    for (int f = 0; f < 2; ++f)
+      for (int f = 0; f < 2; ++f)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int qi = f * 32 + 8 * g + 4 * hf;
-        const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi) * kLog2e;
-        const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + kKT + qi);
+        for (int g = 0; g < 4; ++g) {
+          const int qi = f * 32 + 8 * g + 4 * hf;
+          const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi) * kLog2e;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = q0 + qi + e < S;
-          const float pv = exp2_hw(sv[f][4 * g + e] * c - l4[e]);
-          sv[f][4 * g + e] = ok ? pv : 0.f;
-          dp[f][4 * g + e] = ok ? pv * (dp[f][4 * g + e] - d4[e]) : 0.f;
+          for (int e = 0; e < 4; ++e) {
+            const float pv = exp2_hw(sv[f][4 * g + e] * c - l4[e]);
+            sv[f][4 * g + e] = q0 + qi + e < S ? pv : 0.f;
+            px[(f * 16 + 4 * g + e) * 64 + lane] = sv[f][4 * g + e];
+          }
         }
-      }
+    }
+    lds_barrier();  // P of every group is in LDS
+    if (!role_a) {
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int qi = f * 32 + 8 * g + 4 * hf;
+          const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + kKT + qi);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float pv = px[(f * 16 + 4 * g + e) * 64 + lane];
+            sv[f][4 * g + e] = q0 + qi + e < S ? pv * (sv[f][4 * g + e] - d4[e]) : 0.f;  // dS^T
+          }
+        }
+    }
+    // dV^T += dO^T P (wave A) or dK^T += Q^T dS (wave B)
+    const lds_char *Cs = role_a ? Ds : Qs;
 #pragma unroll
     for (int st = 0; st < kKT / 16; ++st) {
       const bf16x8_t pb = pack8(sv[st >> 1], st & 1);
-      const bf16x8_t sb = pack8(dp[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf) {
-        dv[nf] = mfma32(tile_cols_perm(Ds, nf * 32, st, lane), pb, dv[nf]);
-        dk[nf] = mfma32(tile_cols_perm(Qs, nf * 32, st, lane), sb, dk[nf]);
-      }
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Cs, nf * 32, st, lane), pb, acc[nf]);
     }
-    block_barrier();  // every wave is done with this buffer before it is refilled
+    block_barrier();  // every wave is done with this buffer and the P slots before they are refilled
   }
-  const int k0w = kt * ROWS + wid * 32;
-  bf16_t *row = dqkv + (static_cast<size_t>(b) * S + k0w) * ld + h * D;
-  lds_char *slots = const_cast<lds_char *>(smem);
-  store_dmajor_lds<D>(row + A, ld, dk, 1.0f / sqrtf(static_cast<float>(D)), lane, slots + wid * 8192, S - k0w);
-  store_dmajor_lds<D>(row + 2 * A, ld, dv, 1.0f, lane, slots + (NW + wid) * 8192, S - k0w);
+  // wave A holds dV, wave B dK; the tile buffers are free after the last barrier
+  bf16_t *row = dqkv + (static_cast<size_t>(b) * S + k0w) * ld + h * D + (role_a ? 2 * A : A);
+  store_dmajor_lds<D>(row, ld, acc, role_a ? 1.0f : 1.0f / sqrtf(static_cast<float>(D)), lane,
+                      const_cast<lds_char *>(smem) + wid * 8192, S - k0w);
 }
 
 template <int D>
@@ -554,15 +575,15 @@ void launch_fwd_d(int B, int S, int heads, const bf16_t *qkv, bf16_t *o, float *
 template <int D>
 void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, const float *lse, const bf16_t *dO,
                   bf16_t *dqkv, float *dvec, hipStream_t s) {
-  constexpr int NWQ = 4, NWK = 4;
+  constexpr int NWQ = 4, NGK = 4;
   const uint32_t qkv_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * 3 * heads * D * 2);
   const uint32_t do_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * heads * D * 2);
   const int qblocks = B * heads * ((S + 32 * NWQ - 1) / (32 * NWQ));
-  const int kblocks = B * heads * ((S + 32 * NWK - 1) / (32 * NWK));
-  constexpr int kDqLds = 2 * 2 * kTileBytes, kDkvLds = 2 * (2 * kTileBytes + 2 * kKT * 4);
+  const int kblocks = B * heads * ((S + 32 * NGK - 1) / (32 * NGK));
+  constexpr int kDqLds = 2 * 2 * kTileBytes, kDkvLds = 2 * (2 * kTileBytes + 2 * kKT * 4) + NGK * 8192;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NWQ>), dim3(qblocks), dim3(NWQ * 64), kDqLds, s, B, S, heads,
                      qkv, qkv_bytes, o, lse, dO, dqkv, dvec);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NWK>), dim3(kblocks), dim3(NWK * 64), kDkvLds, s, B, S, heads, qkv,
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NGK>), dim3(kblocks), dim3(NGK * 128), kDkvLds, s, B, S, heads, qkv,
                      qkv_bytes, lse, dO, do_bytes, dvec, dqkv);
 }
 
