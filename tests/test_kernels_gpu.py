@@ -104,10 +104,13 @@ def test_ln_bwd(rows, cols, with_resid):
 # --------------------------------------------------------------------------- GEMM layouts (exact)
 
 # (M, K_in, N_out) covering one tile, many tiles, ragged rows, K not a
-# multiple of the 64-wide k-step (register-staged path) and each tile
-# configuration of the direct-to-LDS path (256x256, 256x192, 128x128).
+# multiple of the 64-wide k-step (register-staged path), each tile
+# configuration of the direct-to-LDS path (256x256, 256x192, 128x128), and
+# both workgroup orders: one contiguous range per XCD (e.g. 16x18 tiles) and
+# XCDs in two halves along M, including a short last group of row tiles
+# (1536x1536: 12x12 tiles, 6 row tiles per half in groups of 4).
 FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
-              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144)]
+              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536)]
 
 
 def _sparse(shape, seed, density):
