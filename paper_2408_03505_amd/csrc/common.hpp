@@ -87,4 +87,13 @@ __device__ __forceinline__ void stg16(bf16_t *p, u32x4_t v) {
   *reinterpret_cast<u32x4_t *>(p) = v;
 }
 
+// Streaming (non-temporal) 16-byte stores, for outputs that the writing
+// kernel does not read again.
+__device__ __forceinline__ void stg16_nt(bf16_t *p, u32x4_t v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t *>(p));
+}
+__device__ __forceinline__ void stg16_nt(float *p, f32x4_t v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t *>(p));
+}
+
 }  // namespace optimus

@@ -139,7 +139,11 @@ __device__ __forceinline__ void store_tile(const GemmArgs &p, const f32x16_t (&a
 // 16-byte row pad (conflict-free for the 64-bank LDS), then every thread
 // streams whole rows out with 16-byte accesses, applying the residual, GELU,
 // GELU' or the fp32 accumulation on the way.  Output rows are written in full
-// 128-byte lines instead of 8-byte pieces scattered over 32 rows.
+// 128-byte lines instead of 8-byte pieces scattered over 32 rows, with
+// non-temporal stores: every CU writes its tile at about the same time, and
+// streaming the burst past the caches measured 2% faster over the layer (the
+// fp32 weight gradients most, and the LayerNorm backward that reads a GEMM
+// output next).
 constexpr int kEpiRows = 64;
 
 template <Epi EPI, int BM, int BN, int WM, int WN>
@@ -189,7 +193,7 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
         f32x4_t v = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc);
         const size_t off = static_cast<size_t>(gm) * p.ldy + gn;
         if (p.accumulate) v += *reinterpret_cast<const f32x4_t *>(p.Wf + off);
-        *reinterpret_cast<f32x4_t *>(p.Wf + off) = v;
+        stg16_nt(p.Wf + off, v);
       }
     } else {
       constexpr int PER_ROW = BN / 8;
@@ -220,11 +224,11 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
         u32x4_t o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = pack2(v[2 * e], v[2 * e + 1]);
-        stg16(p.Y + off, o);
+        stg16_nt(p.Y + off, o);
         if constexpr (EPI == Epi::kBiasGelu) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) o[e] = pack2(gelu_f(v[2 * e]), gelu_f(v[2 * e + 1]));
-          stg16(p.Y2 + off, o);
+          stg16_nt(p.Y2 + off, o);
         }
       }
     }
