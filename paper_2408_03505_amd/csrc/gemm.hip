@@ -33,12 +33,36 @@ namespace optimus {
 
 namespace {
 
-__device__ __forceinline__ float gelu_f(float u) { return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f)); }
+// 1 + erf(x) for the GELU epilogues, from Abramowitz & Stegun, Handbook of
+// Mathematical Functions (1964), formula 7.1.26: for x >= 0,
+// erfc(x) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^(-x^2) with
+// t = 1 / (1 + p x), absolute error <= 1.5e-7.  Then 1 + erf(x) is 2 - erfc(x)
+// for x >= 0 and erfc(-x) for x < 0, so the negative side does not cancel in
+// fp32.  On the hardware reciprocal and exponential this is a fraction of the
+// library erff's instructions; the epilogue evaluates it for every output
+// element, and results are rounded to bf16.  Also returns e^(-x^2), which
+// GELU' needs as well.
+__device__ __forceinline__ float one_plus_erf(float x, float &ex2) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  ex2 = __builtin_amdgcn_exp2f(-(ax * ax) * 1.4426950408889634f);
+  const float erfc_ax = poly * ex2;
+  return x >= 0.0f ? 2.0f - erfc_ax : erfc_ax;
+}
+
+// GELU(u) = u Phi(u) and GELU'(u) = Phi(u) + u phi(u), with
+// Phi(u) = (1 + erf(u / sqrt 2)) / 2 and phi(u) = e^(-u^2 / 2) / sqrt(2 pi).
+__device__ __forceinline__ float gelu_f(float u) {
+  float ex2;
+  return 0.5f * u * one_plus_erf(u * 0.70710678118654752f, ex2);
+}
 
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  const float Phi = 0.5f * (1.0f + erff(u * 0.70710678118654752f));
-  const float phi = expf(-0.5f * u * u) * 0.39894228040143268f;
-  return Phi + u * phi;
+  float ex2;  // e^(-u^2 / 2)
+  const float Phi = 0.5f * one_plus_erf(u * 0.70710678118654752f, ex2);
+  return Phi + u * ex2 * 0.39894228040143268f;
 }
 
 // Logical tile for this workgroup.  MI355X dispatches workgroup i to XCD
@@ -152,11 +176,47 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
   constexpr int NT = WM * WN * 64;
   constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 32, FN = WTN / 32;
   constexpr int LDR = BN + 4;  // floats per LDS row (16-byte pad)
+  constexpr int NCH = BM / kEpiRows;
   static_assert(BM % kEpiRows == 0 && kEpiRows % 32 == 0, "epilogue chunking");
+  constexpr bool kHasBias = EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu;
+  // a second per-element input: the residual, or the saved pre-activation u
+  constexpr bool kHasR = EPI == Epi::kBiasResid || EPI == Epi::kResid || EPI == Epi::kGeluGrad;
+  constexpr int PRB = BN / 8;                        // 16-byte bf16 segments per row
+  constexpr int SEGS = (kEpiRows * PRB + NT - 1) / NT;  // per thread and chunk
   const int tid = threadIdx.x;
   const int lrow = lane & 31;
-#pragma unroll 1
-  for (int c = 0; c < BM / kEpiRows; ++c) {
+
+  // Every load of the epilogue is issued before its first store: loads and
+  // stores retire in issue order, so a load issued behind the stores of the
+  // previous chunk would wait for them.
+  // (the 256-wide tile with both a bias and a residual has no registers to
+  // spare for the bias: it loads the bias per chunk instead)
+  constexpr bool kPreBias = kHasBias && !(kHasR && BN > 192);
+  u32x2_t bias_w[kPreBias ? FN : 1][4];
+  if constexpr (kPreBias) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int nb = n0 + wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
+        bias_w[j][q] = nb < p.N ? *reinterpret_cast<const u32x2_t *>(p.bias + nb) : u32x2_t{0u, 0u};
+      }
+  }
+  u32x4_t rin[kHasR ? NCH : 1][kHasR ? SEGS : 1];
+  if constexpr (kHasR) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int sg = 0; sg < SEGS; ++sg) {
+        const int it = tid + NT * sg;
+        const int gm = m0 + c * kEpiRows + it / PRB, gn = n0 + (it % PRB) * 8;
+        const bool in = it < kEpiRows * PRB && gm < p.M && gn < p.N;
+        rin[c][sg] = in ? ldg16(p.R + static_cast<size_t>(gm) * p.ldy + gn) : u32x4_t{0u, 0u, 0u, 0u};
+      }
+  }
+
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
     __syncthreads();  // LDS free (k-loop reads or the previous chunk's readers done)
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -169,7 +229,12 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
         for (int q = 0; q < 4; ++q) {
           const int cl = wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
           f32x4_t v{acc[i][j][q * 4], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]};
-          if constexpr (EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu) {
+          if constexpr (kPreBias) {
+            v[0] += lo_bf(bias_w[j][q][0]);
+            v[1] += hi_bf(bias_w[j][q][0]);
+            v[2] += lo_bf(bias_w[j][q][1]);
+            v[3] += hi_bf(bias_w[j][q][1]);
+          } else if constexpr (kHasBias) {
             const int nb = n0 + cl;
             if (nb < p.N) {
               const u32x2_t bw = *reinterpret_cast<const u32x2_t *>(p.bias + nb);
@@ -196,29 +261,28 @@ __device__ __forceinline__ void store_tile_lds(const GemmArgs &p, const f32x16_t
         stg16_nt(p.Wf + off, v);
       }
     } else {
-      constexpr int PER_ROW = BN / 8;
-      for (int it = tid; it < kEpiRows * PER_ROW; it += NT) {
-        const int r = it / PER_ROW, cc = (it % PER_ROW) * 8;
+#pragma unroll
+      for (int sg = 0; sg < SEGS; ++sg) {
+        const int it = tid + NT * sg;
+        const int r = it / PRB, cc = (it % PRB) * 8;
         const int gm = m0 + c * kEpiRows + r, gn = n0 + cc;
-        if (gm >= p.M || gn >= p.N) continue;
+        if (it >= kEpiRows * PRB || gm >= p.M || gn >= p.N) continue;
         const f32x4_t a = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc);
         const f32x4_t b = *reinterpret_cast<const f32x4_t *>(lds + r * LDR + cc + 4);
         float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
         const size_t off = static_cast<size_t>(gm) * p.ldy + gn;
         if constexpr (EPI == Epi::kBiasResid || EPI == Epi::kResid) {
-          const u32x4_t rw = ldg16(p.R + off);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            v[2 * e] += lo_bf(rw[e]);
-            v[2 * e + 1] += hi_bf(rw[e]);
+            v[2 * e] += lo_bf(rin[c][sg][e]);
+            v[2 * e + 1] += hi_bf(rin[c][sg][e]);
           }
         }
         if constexpr (EPI == Epi::kGeluGrad) {
-          const u32x4_t uw = ldg16(p.R + off);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            v[2 * e] *= gelu_grad_f(lo_bf(uw[e]));
-            v[2 * e + 1] *= gelu_grad_f(hi_bf(uw[e]));
+            v[2 * e] *= gelu_grad_f(lo_bf(rin[c][sg][e]));
+            v[2 * e + 1] *= gelu_grad_f(hi_bf(rin[c][sg][e]));
           }
         }
         u32x4_t o;

@@ -206,6 +206,42 @@ def test_bwd_data_exact(M, N, K):
         assert ok, err
 
 
+def _bf16_ulp(v):
+    a = np.maximum(np.abs(v), 2.0 ** -126)
+    return 2.0 ** (np.floor(np.log2(a)) - 7)
+
+
+def test_gelu_epilogues_within_one_bf16_ulp():
+    # u = bias exactly (zero activations), so g = GELU(u) and, with a unit
+    # product, du = GELU'(u).  The epilogue's erf is a polynomial
+    # approximation: both must be within one bf16 step of the exact float64
+    # value for u >= -4, and within 1e-6 absolute over [-8, 8] (below -4 the
+    # values are under 1.3e-4 and the approximation's absolute error governs).
+    announce("GELU / GELU' epilogue accuracy")
+    M, K, N = 64, 64, 4096
+    b = torch.linspace(-8.0, 8.0, N).to(torch.bfloat16)
+    X = torch.zeros((M, K), dtype=torch.bfloat16)
+    W = random_bf16((N, K), 71)
+    u, g = B.enc_mlp_up_fwd(cuda(X), cuda(W), cuda(b))
+    # GELU': dout = e_0 rows and W2 row 0 = 1 give a product of exactly 1
+    H = 64
+    dout = torch.zeros((M, H), dtype=torch.bfloat16)
+    dout[:, 0] = 1
+    w2 = torch.zeros((H, N), dtype=torch.bfloat16)
+    w2[0, :] = 1
+    du = B.enc_mlp_down_bwd_data(cuda(dout), cuda(w2), cuda(b.expand(M, N).contiguous()))
+    torch.cuda.synchronize()
+    bu = f64(b)
+    assert np.array_equal(f64(u), np.broadcast_to(bu, (M, N)))
+    main = bu >= -4.0
+    for got, exact in ((f64(g), oracle.gelu(bu)), (f64(du), oracle.gelu_grad(bu))):
+        err = np.abs(got - exact)
+        assert err.max() <= 1e-6 + np.abs(exact).max() * 2.0 ** -8, err.max()
+        ref = f64(torch.from_numpy(exact).to(torch.bfloat16))
+        assert np.all(np.abs(got - ref)[:, main] <= _bf16_ulp(ref)[main]), np.abs(got - ref)[:, main].max()
+        assert np.all(err[:, ~main] <= 1e-6), err[:, ~main].max()
+
+
 def test_mlp_down_bwd_data_gelu_grad():
     announce("mlp_down_bwd_data gelu' epilogue")
     M, H, F = 394, 192, 768
