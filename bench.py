@@ -492,6 +492,124 @@ def corun(chain, p50_alone, dev, steps=5, n=8192):
             "load_tflops_alone": round(load_alone, 1), "load_tflops_corun": round(load_busy, 1)}
 
 
+def cu_mask_words(per_word, words=8):
+    """A CU mask (32-bit words) with per_word bits set in each word, word w
+    holding bits w, w + 8, w + 16, ... (residue w mod 8).  Whichever way the
+    runtime spreads mask bits over MI355X's eight XCDs (32 consecutive bits
+    per XCD, or bit i on XCD i mod 8), every XCD keeps per_word CUs of the
+    mask and 32 - per_word of its complement, so no XCD is left without CUs
+    for either stream."""
+    assert 1 <= per_word <= 4
+    mask = [0] * words
+    for w in range(words):
+        for k in range(per_word):
+            mask[w] |= 1 << (w % 8 + 8 * k)
+    return mask
+
+
+def _hip_runtime():
+    """The HIP runtime library this process already uses (torch's)."""
+    import ctypes
+    paths = sorted({ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln})
+    if not paths:
+        raise RuntimeError("no HIP runtime mapped in this process")
+    return ctypes.CDLL(paths[0])
+
+
+def corun_masked(chain, p50_alone, dev, per_word=4, steps=3, n=8192):
+    """CU-masked co-run: the encoder chain on a stream restricted to a slice
+    of the CUs (per_word bits of every 32-bit mask word: 32 of 256 CUs for
+    per_word = 4) and the GEMM load of corun() on a stream restricted to the
+    complement.  Reports the chain's step time on the slice alone and beside
+    the load, and the load's rate on the complement alone and beside the
+    chain.  Both streams are created with the default priority."""
+    import ctypes
+    hip = _hip_runtime()
+    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                 ctypes.POINTER(ctypes.c_uint32)]
+    hip.hipExtStreamGetCUMask.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint32)]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    ncu = torch.cuda.get_device_properties(dev).multi_processor_count
+    words = (ncu + 31) // 32
+    if words != 8:
+        return {"skipped": f"the mask layout assumes 256 CUs in 8 XCDs (this device has {ncu} CUs)"}
+    enc_mask = cu_mask_words(per_word, words)
+    load_mask = [(~m) & 0xFFFFFFFF for m in enc_mask]
+    handles = []
+
+    def make(mask):
+        arr = (ctypes.c_uint32 * words)(*mask)
+        h = ctypes.c_void_p()
+        err = hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), words, arr)
+        if err != 0:
+            raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({err})")
+        handles.append(h)
+        got = (ctypes.c_uint32 * words)()
+        hip.hipExtStreamGetCUMask(h, words, got)
+        return torch.cuda.ExternalStream(h.value, device=dev), sum(bin(v).count("1") for v in got)
+
+    try:
+        enc, enc_cus = make(enc_mask)
+        load, load_cus = make(load_mask)
+        a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+        b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+        c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+        gemm_flops = 2.0 * n ** 3
+
+        def run_load(k):
+            with torch.cuda.stream(load):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(k):
+                    torch.matmul(a, b, out=c)
+                e1.record()
+            return e0, e1
+
+        def run_chain(k):
+            with torch.cuda.stream(enc):
+                s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                s0.record()
+                for _ in range(k):
+                    for _, fn in chain.kernels:
+                        fn()
+                s1.record()
+            return s0, s1
+
+        torch.cuda.synchronize()
+        run_chain(1)  # warm-up on the slice
+        torch.cuda.synchronize()
+        s0, s1 = run_chain(steps)
+        torch.cuda.synchronize()
+        enc_alone = s0.elapsed_time(s1) / steps
+        run_load(2)
+        torch.cuda.synchronize()
+        e0, e1 = run_load(10)
+        torch.cuda.synchronize()
+        load_alone = 10 * gemm_flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+        k_load = max(10, int(1.5 * steps * enc_alone / (gemm_flops / (load_alone * 1e12) * 1e3)))
+        torch.cuda.synchronize()
+        l0, l1 = run_load(k_load)
+        s0, s1 = run_chain(steps)
+        torch.cuda.synchronize()
+        enc_busy = s0.elapsed_time(s1) / steps
+        load_busy = k_load * gemm_flops / (l0.elapsed_time(l1) * 1e-3) / 1e12
+        covered = l0.elapsed_time(s0) >= 0 and s1.elapsed_time(l1) >= 0
+        step_full = sum(p50_alone.values()) / 1e3
+        return {"encoder_mask": [f"{m:08x}" for m in enc_mask], "encoder_cus": enc_cus, "load_cus": load_cus,
+                "load": f"bf16 GEMM {n}x{n}x{n} (torch.matmul) looped on the complement, {k_load} launches",
+                "load_covers_encoder": bool(covered),
+                "encoder_step_ms_full_gpu": round(step_full, 4),
+                "encoder_step_ms_slice_alone": round(enc_alone, 4),
+                "encoder_step_ms_slice_with_load": round(enc_busy, 4),
+                "slice_isolation": round(enc_busy / enc_alone, 3),
+                "load_tflops_complement_alone": round(load_alone, 1),
+                "load_tflops_complement_with_encoder": round(load_busy, 1)}
+    finally:
+        torch.cuda.synchronize()
+        for h in handles:
+            hip.hipStreamDestroy(h)
+
+
 def time_whole_encoder(cfg, layers, dev, steps=2, warmup=1, img=224, patch=14, channels=3):
     """Forward+backward of a whole ViT encoder on one micro-batch: patch
     embedding of img x img images (no class token), `layers` sequential
@@ -793,6 +911,7 @@ def main():
     res["bubble_fit"] = section(fit_report)
     if not args.no_corun:
         res["corun"] = section(lambda: corun(chain, p50, dev))
+        res["corun_cu_mask"] = section(lambda: corun_masked(chain, p50, dev))
     if not args.no_variants:
         res["variants"] = section(lambda: {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)})
     if args.encoder_layers > 0:

@@ -121,3 +121,19 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     line = json.loads(r.stdout.strip().splitlines()[-1])
     assert "one GPU" in line["error"]
+
+
+def test_cu_mask_leaves_every_xcd_cus_for_both_streams():
+    # the slice and its complement each keep CUs on all eight XCDs whether mask
+    # bits go to XCDs in 32-bit blocks or round-robin by bit index
+    for per_word in (1, 2, 3, 4):
+        mask = bench.cu_mask_words(per_word)
+        comp = [(~m) & 0xFFFFFFFF for m in mask]
+        bits = lambda ws: [32 * w + b for w, m in enumerate(ws) for b in range(32) if (m >> b) & 1]
+        sel, rest = bits(mask), bits(comp)
+        assert len(sel) == 8 * per_word and len(rest) == 256 - 8 * per_word
+        for xcd in range(8):
+            assert sum(1 for i in sel if i // 32 == xcd) == per_word
+            assert sum(1 for i in sel if i % 8 == xcd) == per_word
+            assert sum(1 for i in rest if i // 32 == xcd) == 32 - per_word
+            assert sum(1 for i in rest if i % 8 == xcd) == 32 - per_word
