@@ -799,7 +799,7 @@ def main():
             print(f"| {n} | {fetch[n]:.0f} | {write[n]:.0f} | {t:.0f} | {work[n][1]} | {t / work[n][1]:.2f} |")
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are out of scope "
+        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are out of scope "
                                    "(--gpus must be 1)"}), flush=True)
         sys.exit(2)
     from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs

@@ -16,7 +16,7 @@ them as its reading:
     length head_dim shared by all heads (qn_g, qn_b for queries, kn_g, kn_b
     for keys); values are not normalised;
   - no bias on the QKV projection.
-LayerNorms keep their bias (the survey's reading of this variant); every
+LayerNorms keep their bias (read from the cited ViT-22B architecture); every
 other convention (scale 1/sqrt(d), exact-erf GELU, [3][heads][d] packing,
 epsilon = ln_eps for all LayerNorms) is that of the sequential block.
 """
