@@ -5,8 +5,8 @@
  * work inside the LLM pipeline's idle periods.  Many of those bubbles last
  * well under a millisecond (about 300 us for tensor-parallel bubbles, §2.3,
  * challenge 3), shorter than one encoder layer's forward or backward, so the
- * paper decomposes the encoder layer into a series of kernels and schedules
- * those kernels individually (abstract; §3.1, design decision 3; §4.2, the
+ * paper splits the encoder layer into separately launched kernels and places
+ * each one on its own (abstract; §3.1, design decision 3; §4.2, the
  * ScheduleKernels step, which packs kernels into a bubble while their summed
  * time fits and keeps the encoder's internal order).  Forward and backward are
  * scheduled separately, and the backward may be skipped for a frozen encoder
@@ -406,7 +406,7 @@ int encoder_stack_bwd(const enc_cfg_t *cfg, int layers, const enc_params_t *para
  *
  * The bubble scheduler's ScheduleKernels step (§4.2, fine-grained bubble
  * exploitation): one micro-batch's encoder kernels are placed, in chain
- * order (the encoder's internal data dependencies), into the LLM timeline.
+ * order (each kernel after the one whose output it reads), into the LLM timeline.
  * Computation kernels go into bubbles, several per bubble as long as their
  * summed time fits; communication kernels are not put into bubbles but
  * overlapped with LLM computation (§3.1, design decision 3).  Kernels are

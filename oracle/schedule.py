@@ -7,9 +7,8 @@ The bubble scheduler of the paper (§4.2, fine-grained bubble exploitation,
 the ScheduleKernels step of the BubbleScheduler algorithm) places one
 micro-batch's encoder computation, broken into kernels, into the LLM's
 timeline: several kernels may share one bubble as long as their summed time
-fits in the bubble, the encoder's internal data dependencies are kept (a
-kernel never starts before the one it depends on, i.e. the chain's order is
-kept), and communication kernels are not put into bubbles but overlapped
+fits in the bubble, a kernel never starts before the one whose output it
+reads (the chain's order is kept), and communication kernels are not put into bubbles but overlapped
 with long LLM computation (§3.1, design decision 3; §4.2).
 
 Reading used here (also stated in the design notes): the timeline is a list
