@@ -23,8 +23,9 @@ with one fused QKV projection whose output columns are packed
 eps inside the square root, and the exact (erf) GELU.  The parameter counts
 this gives reproduce the ViT table of Appendix A (tests/golden).  Parameter
 gradients are full sums over all token rows, returned in float64; the GPU
-path keeps them in fp32 because the paper trains with bf16 parameters and
-fp32 gradients (§4.5, memory analysis, k = 6 bytes per parameter).
+path keeps them in fp32 because the paper's training keeps parameters in
+bf16 and their gradients in fp32 (§4.5, memory analysis, k = 6 bytes per
+parameter).
 
 Every array is a numpy float64 array, row-major.  Token rows are M = B*S,
 ordered sequence-major (row r = b*S + s).  Weights are stored [out, in].
