@@ -62,6 +62,9 @@ def parse():
     ap.add_argument("--pmc-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
                          "--copy-mib into per-kernel HBM bytes and print them as markdown")
+    ap.add_argument("--pmc-summary", metavar="DIR",
+                    help="per chain entry, the counters of one rocprofv3 --pmc run of this bench (averaged over "
+                         "its steps) with the matrix-core busy fraction and wait fractions, as markdown")
     return ap.parse_args()
 
 
@@ -146,6 +149,34 @@ def _latest_rows(d, pattern):
 
 def _counter_rows(d):
     return _latest_rows(d, "*counter_collection.csv")
+
+
+def pmc_entries(d):
+    """Per chain entry and counter, the counter's average over the steps of
+    one rocprofv3 --pmc run (each dispatch's value as reported, i.e. summed
+    over the GPU's instances)."""
+    rows = _counter_rows(d)
+    out = {}
+    for ctr in sorted({r["Counter_Name"] for r in rows}):
+        steps = map_dispatches([(int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
+                                for r in rows if r["Counter_Name"] == ctr and is_lib_kernel(r["Kernel_Name"])])
+        for n in DISPATCHES:
+            out.setdefault(n, {})[ctr] = sum(st[n] for st in steps) / len(steps)
+    return out
+
+
+def pmc_utilisation(c, xcds=8, simds=1024):
+    """Derived fractions of one entry's counters: matrix-core busy cycles
+    over (GPU-active cycles of one XCD x SIMDs), and the waves' instruction
+    waits over their cycles."""
+    out = {}
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in c and "GRBM_GUI_ACTIVE" in c:
+        out["mfma_busy"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (c["GRBM_GUI_ACTIVE"] / xcds * simds)
+    if "SQ_WAVE_CYCLES" in c and c["SQ_WAVE_CYCLES"] > 0:
+        for k in ("SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_WAIT_ANY"):
+            if k in c:
+                out[k.lower().replace("sq_", "") + "_per_wave_cycle"] = c[k] / c["SQ_WAVE_CYCLES"]
+    return out
 
 
 def pmc_traffic(fetch_dir, write_dir, copy_bytes):
@@ -783,6 +814,17 @@ def main():
     args = parse()
     if args.summarize:
         summarize(args.summarize, skip_steps=args.warmup)
+        return
+    if args.pmc_summary:
+        ent = pmc_entries(args.pmc_summary)
+        ctrs = sorted({k for v in ent.values() for k in v})
+        derived = sorted({k for n in DISPATCHES for k in pmc_utilisation(ent[n])})
+        print("| entry | " + " | ".join(ctrs + derived) + " |")
+        print("|---" * (1 + len(ctrs) + len(derived)) + "|")
+        for n in DISPATCHES:
+            u = pmc_utilisation(ent[n])
+            print(f"| {n} | " + " | ".join([f"{ent[n][k]:.4g}" for k in ctrs] +
+                                           [f"{u[k]:.3f}" if k in u else "" for k in derived]) + " |")
         return
     if args.pmc_traffic:
         from paper_2408_03505_amd.synthetic import CONFIGS

@@ -137,3 +137,27 @@ def test_cu_mask_leaves_every_xcd_cus_for_both_streams():
             assert sum(1 for i in sel if i % 8 == xcd) == per_word
             assert sum(1 for i in rest if i // 32 == xcd) == 32 - per_word
             assert sum(1 for i in rest if i % 8 == xcd) == 32 - per_word
+
+
+def test_pmc_summary_per_entry_and_busy_fraction(tmp_path):
+    # two steps; per dispatch: MFMA busy 51200 cycles over 8 XCDs x 100 active cycles
+    names = _one_step_names()
+    rows = []
+    for st in range(2):
+        for n in names:
+            rows += [(n, "SQ_VALU_MFMA_BUSY_CYCLES", 512.0 * 100), (n, "GRBM_GUI_ACTIVE", 8 * 100.0),
+                     (n, "SQ_WAVE_CYCLES", 10.0), (n, "SQ_WAIT_ANY", 3.0)]
+    d = tmp_path / "p"
+    os.makedirs(d)
+    with open(d / "1_counter_collection.csv", "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for i, (n, c, v) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i // 4, "Kernel_Name": n, "Counter_Name": c, "Counter_Value": v})
+    ent = bench.pmc_entries(str(d))
+    for n in bench.ENTRY_KERNELS:
+        k = bench.DISPATCHES[n]
+        assert ent[n]["GRBM_GUI_ACTIVE"] == pytest.approx(800.0 * k)
+        u = bench.pmc_utilisation(ent[n])
+        assert u["mfma_busy"] == pytest.approx(0.5)
+        assert u["wait_any_per_wave_cycle"] == pytest.approx(0.3)
