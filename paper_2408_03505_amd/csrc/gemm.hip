@@ -715,22 +715,25 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
     const uint32_t st_l = lds0 + (tl % STAGES) * STAGE;
     // One operand's refill goes out a sub-step after the other's: the
     // activations (A) second in the forward layout (256x192 and 256x256
-    // tiles), the weights (B) second in the input-gradient layout (256x192).
-    // Measured on the ViT-22B layer: QKV forward 8%, MLP-up forward 2% and
-    // the out-projection forward and input gradient 5% faster; later (two
-    // sub-steps) or both operands split in halves was slower.
+    // tiles, contraction up to 8192), the weights (B) second in the
+    // input-gradient layout (256x192).  Measured on the ViT-22B layer: QKV
+    // forward 8%, MLP-up forward 2% and the out-projection forward and input
+    // gradient 5% faster; the forward with K = 24576 (MLP down) was 2% faster
+    // without it; later (two sub-steps) or both operands split in halves was
+    // slower.
     constexpr bool kSpread = !AT && (BT ? BN == 192 : BN >= 192);
     constexpr bool kALate = kSpread && !BT;
+    const bool spread = kSpread && (BT || p.K <= 8192);
     if (tl < nk) {
-      if constexpr (!kALate) la.issue(st_l, tl * a_step, wid);
-      if constexpr (!kSpread || kALate) lb.issue(st_l + A_BYTES, tl * b_step, wid);
+      if (!kALate || !spread) la.issue(st_l, tl * a_step, wid);
+      if (!kSpread || kALate || !spread) lb.issue(st_l + A_BYTES, tl * b_step, wid);
     }
     const lds_char *As = smem + (t % STAGES) * STAGE;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int c = kk & 1, n = c ^ 1;
       if constexpr (kSpread) {
-        if (kk == 1 && tl < nk) {
+        if (kk == 1 && tl < nk && spread) {
           if constexpr (kALate)
             la.issue(st_l, tl * a_step, wid);
           else
