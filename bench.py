@@ -50,6 +50,8 @@ def parse():
                          "at the workload's shape; 0 skips it")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip timing the layer chain at the other workloads (ViT-Tiny/Base/Huge, TP shard)")
+    ap.add_argument("--no-isolated", action="store_true",
+                    help="skip timing every kernel on its own, launched back to back")
     ap.add_argument("--no-flush", action="store_true",
                     help="skip timing the memory-bound kernels after a 512 MiB cache flush")
     ap.add_argument("--no-ceilings", action="store_true",
@@ -353,6 +355,27 @@ def time_chain(chain, steps, warmup):
     torch.cuda.synchronize()
     return {n: float(np.median([ev[k][i][0].elapsed_time(ev[k][i][1]) * 1e3 for k in range(steps)]))
             for i, n in enumerate(names)}
+
+
+def time_isolated(chain, p50_chain, reps=20, warmup=3):
+    """Every chain entry launched reps times back to back on its own (its
+    inputs stay warm in the caches), p50 and p90 in us, beside its p50
+    inside the chain."""
+    out = {}
+    for n, fn in chain.kernels:
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        us = [a.elapsed_time(b) * 1e3 for a, b in ev]
+        out[n] = {"p50_us": round(float(np.median(us)), 2), "p90_us": round(float(np.percentile(us, 90)), 2),
+                  "chain_p50_us": round(p50_chain[n], 2)}
+    return out
 
 
 MEM_BOUND = ("ln1_fwd", "ln2_fwd", "ln2_bwd", "ln1_bwd")
@@ -958,6 +981,8 @@ def main():
         res["variants"] = section(lambda: {f"{args.config}_parallel_block": time_parallel_block(cfg, dev)})
     if args.encoder_layers > 0:
         res["whole_encoder"] = section(lambda: time_whole_encoder(cfg, args.encoder_layers, dev))
+    if not args.no_isolated:
+        res["isolated"] = section(lambda: time_isolated(chain, p50))
     if not args.no_flush:
         res["memory_bound"] = section(lambda: time_flushed(chain, work))
     if not args.no_configs:
