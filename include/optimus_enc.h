@@ -299,6 +299,8 @@ typedef struct {
   size_t total;
 } enc_psaved_layout_t;
 
+/* Fills layout with the offsets above for cfg (16-byte aligned, disjoint);
+ * ENC_ERR_INVALID / ENC_ERR_UNSUPPORTED for a bad cfg. */
 int enc_parallel_saved_layout(const enc_cfg_t *cfg, enc_psaved_layout_t *layout);
 /* Workspace bytes encoder_parallel_bwd needs. */
 int enc_parallel_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes);
@@ -330,6 +332,8 @@ int enc_qk_norm_fwd(int M, int heads, int head_dim, const enc_bf16 *qkv,
                     const enc_bf16 *kn_g, const enc_bf16 *kn_b, float eps,
                     enc_bf16 *qkvn, float *stats, enc_stream_t stream);
 
+/* Workspace bytes enc_qk_norm_bwd needs (per-block partial sums of the four
+ * affine gradients, reduced in a fixed order). */
 int enc_qk_norm_bwd_workspace_bytes(int M, int heads, int head_dim, size_t *bytes);
 
 /* Gradient of enc_qk_norm_fwd: dqkv from dqkvn (LayerNorm backward for
