@@ -299,7 +299,7 @@ typedef struct {
   size_t total;
 } enc_psaved_layout_t;
 
-/* Fills layout with the offsets above for cfg (16-byte aligned, disjoint);
+/* Fills layout with the offsets above for cfg (256-byte aligned, disjoint);
  * ENC_ERR_INVALID / ENC_ERR_UNSUPPORTED for a bad cfg. */
 int enc_parallel_saved_layout(const enc_cfg_t *cfg, enc_psaved_layout_t *layout);
 /* Workspace bytes encoder_parallel_bwd needs. */
