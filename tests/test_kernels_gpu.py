@@ -110,7 +110,7 @@ def test_ln_bwd(rows, cols, with_resid):
 # XCDs in two halves along M, including a short last group of row tiles
 # (1536x1536: 12x12 tiles, 6 row tiles per half in groups of 4).
 FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
-              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536)]
+              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536), (2048, 64, 24576)]
 
 
 def _sparse(shape, seed, density):
