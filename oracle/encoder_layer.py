@@ -31,12 +31,14 @@ Every array is a numpy float64 array, row-major.  Token rows are M = B*S,
 ordered sequence-major (row r = b*S + s).  Weights are stored [out, in].
 
 Each function is written from its mathematical definition with numpy's
-matmul as the only library primitive; nothing is blocked, fused or reordered.
+matmul and scipy's erf as the only library primitives; nothing is blocked,
+fused or reordered.
 """
 
 import math
 
 import numpy as np
+import scipy.special
 
 __all__ = [
     "layernorm_fwd",
@@ -140,7 +142,9 @@ def linear_bwd_weight(dY, X):
 
 # ---------------------------------------------------------------- GELU
 
-_erf = np.vectorize(math.erf, otypes=[np.float64])
+# The error function, element-wise in float64 (scipy's vectorised erf; agrees
+# with math.erf to within 5e-16 relative).
+_erf = scipy.special.erf
 
 
 def gelu(u):
