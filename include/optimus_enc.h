@@ -127,7 +127,12 @@ int enc_attn_bwd_workspace_bytes(int batch, int seq, int heads, int head_dim, si
 
 /* ------------------------------------------------------------ composites */
 
-/* Forward of one pre-LN encoder layer on one micro-batch: the kernels of
+/* [One micro-batch of one encoder layer, as one scheduling unit (§4.2);
+ * the chain of the kernels below (§3.1 decision 3)]
+ * Both composites check every argument, and every shape limit of every
+ * kernel they launch, before the first launch: a status other than ENC_OK
+ * and ENC_ERR_LAUNCH means nothing was enqueued.
+ * Forward of one pre-LN encoder layer on one micro-batch: the kernels of
  * the forward chain in order (LN1, QKV projection, attention, output
  * projection + residual, LN2, MLP up + GELU, MLP down + residual) on one
  * stream.  x, out: [M, H].  saved: enc_saved_layout().total bytes, filled
@@ -147,9 +152,20 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params,
                       const enc_grads_t *grads, int accumulate,
                       void *ws, size_t ws_bytes, enc_stream_t stream);
 
-/* ------------------------------------------------------------ forward kernels */
+/* ------------------------------------------------------------ forward kernels
+ *
+ * One entry point per kernel of the layer's decomposition.  The paper
+ * splits the encoder layer into kernels so that each one can be placed in a
+ * bubble on its own (§3.1, design decision 3; §4.2, ScheduleKernels), but
+ * it does not write the layer out: it names the encoders (Appendix A, ViT
+ * table: width, MLP dimension, heads, head dimension).  The layer these
+ * kernels compute is the pre-LN ViT block of those encoders,
+ *   h = x + Attn(LN1(x)) w_o^T + b_o,  out = h + GELU(LN2(h) w_1^T + b_1) w_2^T + b_2,
+ * whose parameter count, 4H^2 + 2HF per layer, reproduces the table's model
+ * sizes.  Each declaration below names its step of that block. */
 
-/* LayerNorm over each of `rows` rows of `cols` values: per row the mean and
+/* [Block steps LN1 and LN2 (Appendix A encoders; §3.1 decision 3)]
+ * LayerNorm over each of `rows` rows of `cols` values: per row the mean and
  * biased variance, rstd = 1/sqrt(var + eps), y = (x - mean)*rstd*gamma + beta.
  * x, y: [rows, cols] bf16; gamma, beta: [cols] bf16; mean, rstd: [rows] fp32
  * (kept for the backward).  cols must be a multiple of 8 and <= 16384. */
@@ -157,12 +173,14 @@ int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma,
                const enc_bf16 *beta, float eps, enc_bf16 *y, float *mean,
                float *rstd, enc_stream_t stream);
 
-/* QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A].
+/* [Block step: fused Q, K, V projection (Appendix A heads x head dim; §3.1 decision 3)]
+ * QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A].
  * b_qkv may be NULL (no bias, as in the ViT-22B-style block below). */
 int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv,
                 const enc_bf16 *b_qkv, enc_bf16 *qkv, enc_stream_t stream);
 
-/* Bidirectional softmax attention of every (sequence, head): for queries i
+/* [Block step: multi-head self-attention (Appendix A heads x head dim; §3.1 decision 3)]
+ * Bidirectional softmax attention of every (sequence, head): for queries i
  * and keys j of one sequence, P = softmax_j(q_i . k_j / sqrt(head_dim)),
  * o_i = sum_j P_ij v_j.  qkv: [batch*seq, 3*heads*head_dim] as written by
  * enc_qkv_fwd; o: [batch*seq, heads*head_dim]; lse: [batch, heads, seq] fp32,
@@ -171,46 +189,59 @@ int enc_attn_fwd(int batch, int seq, int heads, int head_dim,
                  const enc_bf16 *qkv, enc_bf16 *o, float *lse,
                  enc_stream_t stream);
 
-/* Output projection with residual: h[M, H] = resid[M, H] + o[M, A] *
+/* [Block step: attention output projection + residual (§3.1 decision 3)]
+ * Output projection with residual: h[M, H] = resid[M, H] + o[M, A] *
  * w_o[H, A]^T + b_o[H]. */
 int enc_oproj_fwd(int M, int A, int H, const enc_bf16 *o, const enc_bf16 *w_o,
                   const enc_bf16 *b_o, const enc_bf16 *resid, enc_bf16 *h,
                   enc_stream_t stream);
 
-/* MLP up-projection with GELU: u[M, F] = y2[M, H] * w_1[F, H]^T + b_1[F];
+/* [Block step: MLP up-projection to the MLP dimension of Appendix A, GELU (§3.1 decision 3)]
+ * MLP up-projection with GELU: u[M, F] = y2[M, H] * w_1[F, H]^T + b_1[F];
  * g = GELU(u) = u * Phi(u) (exact erf form).  Both u and g are written
  * (u is kept for the backward). */
 int enc_mlp_up_fwd(int M, int H, int F, const enc_bf16 *y2, const enc_bf16 *w_1,
                    const enc_bf16 *b_1, enc_bf16 *u, enc_bf16 *g,
                    enc_stream_t stream);
 
-/* MLP down-projection with residual: out[M, H] = resid[M, H] + g[M, F] *
+/* [Block step: MLP down-projection + residual (§3.1 decision 3)]
+ * MLP down-projection with residual: out[M, H] = resid[M, H] + g[M, F] *
  * w_2[H, F]^T + b_2[H]. */
 int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2,
                      const enc_bf16 *b_2, const enc_bf16 *resid, enc_bf16 *out,
                      enc_stream_t stream);
 
-/* ------------------------------------------------------------ backward kernels */
+/* ------------------------------------------------------------ backward kernels
+ *
+ * The backward of the same block, one kernel per step, scheduled apart from
+ * the forward (§4.2; the backward may be skipped for a frozen encoder, §6).
+ * Parameter gradients are fp32 (bf16 parameters with fp32 gradients, §4.5
+ * memory analysis). */
 
-/* MLP down input gradient through GELU: du[M, F] = (dout[M, H] * w_2[H, F])
+/* [Backward of the MLP down-projection and GELU (§3.1 decision 3; §4.2)]
+ * MLP down input gradient through GELU: du[M, F] = (dout[M, H] * w_2[H, F])
  * * GELU'(u), GELU'(u) = Phi(u) + u*phi(u); u is the saved pre-activation. */
 int enc_mlp_down_bwd_data(int M, int F, int H, const enc_bf16 *dout,
                           const enc_bf16 *w_2, const enc_bf16 *u, enc_bf16 *du,
                           enc_stream_t stream);
 
-/* MLP up input gradient: dy2[M, H] = du[M, F] * w_1[F, H]. */
+/* [Backward of the MLP up-projection, input side (§3.1 decision 3; §4.2)]
+ * MLP up input gradient: dy2[M, H] = du[M, F] * w_1[F, H]. */
 int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du,
                         const enc_bf16 *w_1, enc_bf16 *dy2, enc_stream_t stream);
 
-/* Output projection input gradient: do_[M, A] = dh[M, H] * w_o[H, A]. */
+/* [Backward of the output projection, input side (§3.1 decision 3; §4.2)]
+ * Output projection input gradient: do_[M, A] = dh[M, H] * w_o[H, A]. */
 int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh,
                        const enc_bf16 *w_o, enc_bf16 *do_, enc_stream_t stream);
 
-/* QKV projection input gradient: dy1[M, H] = dqkv[M, 3A] * w_qkv[3A, H]. */
+/* [Backward of the QKV projection, input side (§3.1 decision 3; §4.2)]
+ * QKV projection input gradient: dy1[M, H] = dqkv[M, 3A] * w_qkv[3A, H]. */
 int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv,
                      const enc_bf16 *w_qkv, enc_bf16 *dy1, enc_stream_t stream);
 
-/* Parameter gradients of a linear layer Y = X W^T + b, summed over the M
+/* [Backward of the four projections, parameter side; fp32 gradients (§4.5)]
+ * Parameter gradients of a linear layer Y = X W^T + b, summed over the M
  * token rows: dW[N, K] = dY[M, N]^T * X[M, K]; db[N] = sum_m dY[m, :]
  * (db may be NULL).  fp32 outputs are overwritten (accumulate=0) or added
  * to (accumulate=1).  The sums are deterministic (no atomics). */
@@ -235,7 +266,8 @@ int enc_qkv_bwd_weight(int M, int H, int A, const enc_bf16 *dqkv,
                        const enc_bf16 *y1, float *dw_qkv, float *db_qkv,
                        int accumulate, enc_stream_t stream);
 
-/* LayerNorm backward (exact gradient of enc_ln_fwd) with the residual
+/* [Backward of LN2 and LN1 with the residual branch (§3.1 decision 3; §4.2)]
+ * LayerNorm backward (exact gradient of enc_ln_fwd) with the residual
  * branch added: with xhat = (x - mean)*rstd and ghat = dy*gamma, per row
  * dx = dresid + rstd*(ghat - mean(ghat) - xhat*mean(ghat*xhat)); and over
  * all rows dgamma = sum dy*xhat, dbeta = sum dy (fp32, overwritten or
@@ -248,7 +280,8 @@ int enc_ln_bwd(int rows, int cols, const enc_bf16 *dy, const enc_bf16 *x,
                float *dbeta, int accumulate, void *ws, size_t ws_bytes,
                enc_stream_t stream);
 
-/* Attention backward (exact gradient of enc_attn_fwd): with P recomputed
+/* [Backward of the self-attention step (§3.1 decision 3; §4.2)]
+ * Attention backward (exact gradient of enc_attn_fwd): with P recomputed
  * from lse, D_i = sum_e do_ie*o_ie, dV = P^T dO, dP = dO V^T,
  * dS = P*(dP - D), dQ = dS K/sqrt(d), dK = dS^T Q/sqrt(d), written to
  * dqkv [batch*seq, 3*heads*head_dim] in the qkv packing.  ws holds D

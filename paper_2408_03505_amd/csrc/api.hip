@@ -78,12 +78,32 @@ int check_mult8(const char *fn, std::initializer_list<int> dims) {
 // but tile indices and row counts are 32-bit).
 constexpr long kMaxElems = 1L << 31;
 
+// A launcher refused a shape that the argument checks accepted.  The checks
+// cover every refusal condition (check_cfg), so this is unreachable; if it
+// ever happens, kernels of the same call may already be enqueued, which is
+// what ENC_ERR_LAUNCH reports.
+int refused_after_checks(const char *fn) {
+  return fail(ENC_ERR_LAUNCH, "%s: internal error: a kernel refused a shape the argument checks accepted", fn);
+}
+
 int launched(const char *fn) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(ENC_ERR_LAUNCH, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   return ok();
 }
 
+// The attention kernels address qkv, plus one 64-token tile of overhang and a
+// 256-byte row tail, with 32-bit byte offsets into a buffer resource.
+bool attn_addressable(uint64_t tokens, uint64_t heads, uint64_t d) {
+  return (tokens + 64) * 3 * heads * d * 2 + 256 < (1ull << 32);
+}
+
+// Every refusal condition of every kernel a layer composite launches is
+// checked here, so that a composite that passes check_cfg (and its pointer
+// and workspace checks) launches its whole chain: the GEMM launchers always
+// have a kernel (the register-staged one covers every multiple of 8), the
+// LayerNorm kernels cover widths up to 16384, and attention is limited by
+// head_dim and by attn_addressable.
 int check_cfg(const char *fn, const enc_cfg_t *c) {
   if (!c) return fail(ENC_ERR_INVALID, "%s: cfg is NULL", fn);
   int r = check_dims(fn, {c->batch, c->seq, c->hidden, c->heads, c->head_dim, c->mlp});
@@ -98,6 +118,8 @@ int check_cfg(const char *fn, const enc_cfg_t *c) {
   if (M * c->mlp >= kMaxElems || M * 3 * A >= kMaxElems || M * c->hidden >= kMaxElems ||
       static_cast<long>(c->mlp) * c->hidden >= kMaxElems)
     return fail(ENC_ERR_UNSUPPORTED, "%s: a tensor exceeds 2^31 elements", fn);
+  if (!attn_addressable(static_cast<uint64_t>(M), c->heads, c->head_dim))
+    return fail(ENC_ERR_UNSUPPORTED, "%s: qkv exceeds the 4 GiB the attention kernels address", fn);
   return ENC_OK;
 }
 
@@ -238,8 +260,7 @@ int attn_dims(const char *fn, int B, int S, int heads, int d) {
   if (d != 64 && d != 80 && d != 128) return fail(ENC_ERR_UNSUPPORTED, "%s: head_dim must be 64, 80 or 128", fn);
   if (static_cast<long>(B) * S * 3 * heads * d >= kMaxElems)
     return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
-  // the attention kernels address qkv (plus one tile of overhang) with 32-bit byte offsets
-  if ((static_cast<uint64_t>(B) * S + 64) * 3 * heads * d * 2 + 256 >= (1ull << 32))
+  if (!attn_addressable(static_cast<uint64_t>(B) * S, heads, d))
     return fail(ENC_ERR_UNSUPPORTED, "%s: qkv exceeds the 4 GiB the attention kernels address", fn);
   return ENC_OK;
 }
@@ -436,7 +457,7 @@ int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma, con
   c.req(x, "x").req(gamma, "gamma").req(beta, "beta").req(y, "y").req(mean, "mean").req(rstd, "rstd");
   if (c.code) return c.code;
   if (!launch_ln_fwd(rows, cols, x, gamma, beta, eps, y, mean, rstd, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -620,7 +641,7 @@ int enc_ln_bwd(int rows, int cols, const enc_bf16 *dy, const enc_bf16 *x, const 
     return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, ln_bwd_ws_bytes(rows, cols));
   if (!launch_ln_bwd(rows, cols, dy, x, mean, rstd, gamma, dresid, dx, dgamma, dbeta, accumulate ? 1 : 0,
                      static_cast<float *>(ws), as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -671,7 +692,7 @@ int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   okk = okk && launch_ln_fwd(M, H, h, p.ln2_g, p.ln2_b, cfg->ln_eps, y2, mean2, rstd2, s);
   okk = okk && gemm_fwd(M, F, H, y2, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);
   okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -715,7 +736,7 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, s);       // dy1 = dqkv Wqkv
   okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, s);  // dWqkv, dbqkv
   okk = okk && launch_ln_bwd(M, H, dy1, x, mean1, rstd1, p.ln1_g, dh, dx, gr.ln1_g, gr.ln1_b, acc, part, s);
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -808,7 +829,7 @@ int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, s);   // x + attention branch
   okk = okk && gemm_fwd(M, F, H, y, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);    // MLP reads y too
   okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);  // + MLP branch
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -852,7 +873,7 @@ int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y, gr.w_qkv, nullptr, acc, s);  // dWqkv (no bias)
   okk = okk && gemm_dgrad_add(M, 3 * A, H, dqkv, p.w_qkv, dy_mlp, dy, s);   // dy = dqkv Wqkv + dy_mlp
   okk = okk && launch_ln_bwd(M, H, dy, x, mean, rstd, p.ln_g, dout, dx, gr.ln_g, gr.ln_b, acc, ln_part, s);
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -888,7 +909,7 @@ int enc_patch_embed_fwd(int batch, int channels, int img_h, int img_w, int patch
   bool okk = launch_patchify(batch, channels, img_h, img_w, patch, Kp, images, patches, s);
   okk = okk && gemm_fwd(batch * N, hidden, Kp, patches, w_pe, b_pe, nullptr, tok, nullptr, Epi::kBias, s);
   okk = okk && launch_patch_assemble(batch, N, S, hidden, has_cls, tok, cls, pos, x0, s);
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -914,7 +935,7 @@ int enc_patch_embed_bwd(int batch, int channels, int img_h, int img_w, int patch
     dtok = static_cast<const bf16_t *>(ws);
   }
   okk = okk && gemm_wgrad(batch * N, hidden, Kp, dtok, patches, dw_pe, db_pe, acc, s);
-  if (!okk) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel for this shape", fn);
+  if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -962,7 +983,7 @@ int encoder_stack_fwd(const enc_cfg_t *cfg, int layers, const enc_params_t *para
   }
   if (!launch_ln_fwd(M, cfg->hidden, x, lnf_g, lnf_b, cfg->ln_eps, out, at<float>(saved, L.mean),
                      at<float>(saved, L.rstd), as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -992,7 +1013,7 @@ int encoder_stack_bwd(const enc_cfg_t *cfg, int layers, const enc_params_t *para
   const enc_bf16 *xL = at<enc_bf16>(saved, L.x_step * (layers - 1));
   if (!launch_ln_bwd(M, cfg->hidden, dout, xL, at<float>(saved, L.mean), at<float>(saved, L.rstd), lnf_g, nullptr,
                      bufs[0], dlnf_g, dlnf_b, accumulate ? 1 : 0, at<float>(ws, W.ln_part), s))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: unsupported width", fn);
+    return refused_after_checks(fn);
   if ((r = launched(fn))) return r;
   int cur = 0;
   for (int l = layers - 1; l >= 0; --l) {

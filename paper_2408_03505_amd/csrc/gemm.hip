@@ -986,9 +986,14 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 // (tile area / per-tile efficiency).  Measured on MI355X at the ViT-22B layer
 // shapes with random bf16 data: 256x256 tiles are the most efficient per
 // tile, 256x192 tiles divide the 6144- and 18432-wide outputs into whole
-// rounds, 128x128 tiles serve small problems.  Kernels whose B operand is
-// contraction-strided (input and weight gradients) run the ping-pong
-// schedule (BK = 32, 4 stages), which hides their transpose reads better.
+// rounds, 128x128 tiles serve small problems.  Kernel per tile and layout:
+//   tile      forward (A, B k-contiguous)  input gradient (B strided)  weight gradient (both strided)
+//   256x256   gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage  gemm_pp_kernel BK32 4-stage
+//   256x192   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage
+//   128x128   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage
+// The ping-pong schedule hides the transpose reads of strided operands
+// better where it is used; on the 256x192 input gradients it measured no
+// better than the two-stage kernel.
 // Returns false when the operands do not fit the path's constraints.
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s) {

@@ -118,6 +118,43 @@ def test_bad_configs_are_rejected():
 
 FAKE = 0x10000  # aligned, never dereferenced
 
+# Every tensor under 2^31 elements (M * 3A = 2147481600), but qkv plus the
+# attention kernels' one-tile overhang past the 4 GiB of 32-bit byte offsets.
+NEAR_LIMIT = dict(batch=1, seq=5592400, hidden=8, heads=1, head_dim=128, mlp=8, ln_eps=1e-6)
+
+
+def test_attention_address_limit_is_a_cfg_check():
+    for query in (B.layer_workspace_bytes, B.saved_layout, B.parallel_workspace_bytes, B.parallel_saved_layout):
+        with pytest.raises(B.EncError) as e:
+            query(NEAR_LIMIT)
+        assert e.value.status == B.ENC_ERR_UNSUPPORTED and "4 GiB" in str(e.value), query
+    # one fewer token of overhang room fits
+    ok = dict(NEAR_LIMIT, seq=NEAR_LIMIT["seq"] - 64)
+    assert B.layer_workspace_bytes(ok) > 0
+
+
+@no_gpu_only
+def test_composites_refuse_before_launching():
+    # The composites validate every kernel's shape limits before the first
+    # launch; with fake pointers a launch would fault, so a clean
+    # ENC_ERR_UNSUPPORTED shows that nothing was enqueued.
+    p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
+    cfg = B.make_cfg(NEAR_LIMIT)
+    params = B.EncParams(*[FAKE] * 12)
+    grads = B.EncGrads(*[FAKE] * 12)
+    assert _status("encoder_layer_fwd", ctypes.byref(cfg), ctypes.byref(params), p, p, p, p, 0, s) \
+        == B.ENC_ERR_UNSUPPORTED
+    assert _status("encoder_layer_bwd", ctypes.byref(cfg), ctypes.byref(params), p, p, p, p, ctypes.byref(grads),
+                   1, p, 1 << 40, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("encoder_stack_fwd", ctypes.byref(cfg), 2, (B.EncParams * 2)(params, params), p, p, p, p, p, s) \
+        == B.ENC_ERR_UNSUPPORTED
+    pp = B.EncPParams(*[FAKE] * 13)
+    pg = B.EncPGrads(*[FAKE] * 13)
+    assert _status("encoder_parallel_fwd", ctypes.byref(cfg), ctypes.byref(pp), p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("encoder_parallel_bwd", ctypes.byref(cfg), ctypes.byref(pp), p, p, p, p, ctypes.byref(pg), 1, p,
+                   1 << 40, s) == B.ENC_ERR_UNSUPPORTED
+    assert b"4 GiB" in B.lib().enc_last_error()
+
 
 @no_gpu_only
 def test_null_and_misaligned_pointers_are_rejected():
