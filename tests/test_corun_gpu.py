@@ -9,11 +9,14 @@ so the bar is bit equality.
 
 Two settings, each against the chain run alone on an idle GPU:
   * co-run: the per-kernel chain on one stream while a loop of bf16 GEMMs
-    (torch.matmul, standing in for the LLM's computation) runs on another;
+    (torch.matmul, standing in for the LLM's computation) runs on another,
+    both streams allowed on every CU;
   * CU-masked co-run: the same pair on two streams restricted to
-    complementary CU sets (hipExtStreamCreateWithCUMask), 32 CUs for the
-    encoder (4 in every XCD) and the other 224 for the load.
-Both streams keep the default priority.
+    complementary CU sets, 32 CUs for the encoder (4 in every XCD) and the
+    other 224 for the load.
+Both streams are made by hipExtStreamCreateWithCUMask (a full mask for the
+plain co-run), which gives each its own hardware queue, and keep the default
+priority.  Each test also checks that the load spans the chain.
 """
 
 import ctypes
@@ -129,31 +132,6 @@ def _gemm_ms(stream, a, b, c):
     return e0.elapsed_time(e1) / 5
 
 
-@pytest.mark.parametrize("name", ["vit_huge", "vit22b_tp8"])
-def test_chain_bit_equal_beside_gemm_load(name):
-    announce(f"co-run bit equality {name}")
-    chain, a, b, c = _setup(name)
-    enc, load = torch.cuda.Stream(), torch.cuda.Stream()
-    chain.clear()
-    torch.cuda.synchronize()
-    s0, s1 = _timed_chain(chain, enc)
-    torch.cuda.synchronize()
-    ref = chain.snapshot()
-    alone_ms = s0.elapsed_time(s1)
-    # enough load to outlast the chain even if sharing the GPU slows it fiftyfold
-    # (its short LayerNorm kernels wait behind whole-chip GEMM workgroups)
-    k = max(10, int(50 * alone_ms / _gemm_ms(load, a, b, c)) + 1)
-    for rep in range(2):
-        chain.clear()
-        torch.cuda.synchronize()
-        l0, l1 = _load(load, a, b, c, k)
-        s0, s1 = _timed_chain(chain, enc)
-        torch.cuda.synchronize()
-        _assert_bit_equal(chain.snapshot(), ref, f"co-run {name} rep {rep}")
-        # the load started before the chain and ended after it: they shared the GPU
-        assert l0.elapsed_time(s0) >= 0 and s1.elapsed_time(l1) >= 0, (k, alone_ms)
-
-
 def _hip_runtime():
     """The HIP runtime library torch already loaded into this process."""
     paths = sorted({ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln})
@@ -165,56 +143,104 @@ def _hip_runtime():
     return hip
 
 
+class MaskedStreams:
+    """Streams created with a CU mask (default priority).  Each such stream
+    gets a hardware queue of its own, so two of them really run side by side;
+    plain streams may share one of the process's few hardware queues and
+    then run one after the other."""
+
+    def __init__(self):
+        self.hip = _hip_runtime()
+        self.handles = []
+
+    def make(self, mask):
+        arr = (ctypes.c_uint32 * len(mask))(*mask)
+        h = ctypes.c_void_p()
+        err = self.hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), len(mask), arr)
+        assert err == 0, f"hipExtStreamCreateWithCUMask failed ({err})"
+        self.handles.append(h)
+        return torch.cuda.ExternalStream(h.value)
+
+    def close(self):
+        torch.cuda.synchronize()
+        for h in self.handles:
+            self.hip.hipStreamDestroy(h)
+
+
 def _encoder_mask(words=8, per_word=4):
     """per_word bits of every 32-bit word, word w holding bits w, w+8, ...,
     so each XCD keeps CUs of both sets whichever way mask bits map to XCDs."""
     return [sum(1 << (w % 8 + 8 * k) for k in range(per_word)) for w in range(words)]
 
 
-@pytest.mark.parametrize("name", ["vit22b_tp8"])
-def test_chain_bit_equal_on_cu_masked_streams(name):
+def _cu_words():
     ncu = torch.cuda.get_device_properties(0).multi_processor_count
     if ncu != 256:
         pytest.skip(f"the mask layout assumes 256 CUs in 8 XCDs (device has {ncu})")
-    announce(f"CU-masked co-run bit equality {name}")
-    chain, a, b, c = _setup(name)
-    torch.cuda.synchronize()
+    return 8
+
+
+def _corun(chain, enc, load, a, b, c, ref, what, factor):
+    """Chain alone on enc, then beside a GEMM loop on load sized to outlast
+    it `factor` times over; both runs must equal ref bit for bit."""
     chain.clear()
-    plain = torch.cuda.Stream()
-    chain.run(plain)
+    torch.cuda.synchronize()
+    s0, s1 = _timed_chain(chain, enc)
+    torch.cuda.synchronize()
+    _assert_bit_equal(chain.snapshot(), ref, f"{what}: chain alone")
+    alone_ms = s0.elapsed_time(s1)
+    k = max(10, int(factor * alone_ms / _gemm_ms(load, a, b, c)) + 1)
+    chain.clear()
+    torch.cuda.synchronize()
+    l0, l1 = _load(load, a, b, c, k)
+    s0, s1 = _timed_chain(chain, enc)
+    torch.cuda.synchronize()
+    _assert_bit_equal(chain.snapshot(), ref, f"{what}: beside the load")
+    timeline = dict(load_ms=l0.elapsed_time(l1), chain_start_ms=l0.elapsed_time(s0),
+                    chain_end_ms=l0.elapsed_time(s1), chain_alone_ms=alone_ms, gemms=k)
+    # the load started before the chain and ended after it: they shared the GPU
+    assert timeline["chain_start_ms"] >= 0 and timeline["chain_end_ms"] <= timeline["load_ms"], timeline
+    print(f"[corun] {what}: {timeline}", flush=True)
+
+
+@pytest.mark.parametrize("name", ["vit_huge", "vit22b_tp8"])
+def test_chain_bit_equal_beside_gemm_load(name):
+    words = _cu_words()
+    announce(f"co-run bit equality {name}")
+    chain, a, b, c = _setup(name)
+    chain.clear()
+    torch.cuda.synchronize()
+    chain.run(torch.cuda.current_stream())
     torch.cuda.synchronize()
     ref = chain.snapshot()
-    hip = _hip_runtime()
-    handles = []
-
-    def make(mask):
-        arr = (ctypes.c_uint32 * len(mask))(*mask)
-        h = ctypes.c_void_p()
-        err = hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), len(mask), arr)
-        assert err == 0, f"hipExtStreamCreateWithCUMask failed ({err})"
-        handles.append(h)
-        return torch.cuda.ExternalStream(h.value)
-
+    st = MaskedStreams()
     try:
-        enc_mask = _encoder_mask()
-        enc = make(enc_mask)
-        load = make([(~m) & 0xFFFFFFFF for m in enc_mask])
-        # the chain alone on its slice
-        chain.clear()
-        torch.cuda.synchronize()
-        s0, s1 = _timed_chain(chain, enc)
-        torch.cuda.synchronize()
-        _assert_bit_equal(chain.snapshot(), ref, f"masked slice alone {name}")
-        alone_ms = s0.elapsed_time(s1)
-        k = max(10, int(1.5 * alone_ms / _gemm_ms(load, a, b, c)) + 1)
-        chain.clear()
-        torch.cuda.synchronize()
-        l0, l1 = _load(load, a, b, c, k)
-        s0, s1 = _timed_chain(chain, enc)
-        torch.cuda.synchronize()
-        _assert_bit_equal(chain.snapshot(), ref, f"masked co-run {name}")
-        assert l0.elapsed_time(s0) >= 0 and s1.elapsed_time(l1) >= 0, (k, alone_ms)
+        full = [0xFFFFFFFF] * words
+        enc, load = st.make(full), st.make(full)
+        # enough load to outlast the chain even if sharing the GPU slows it fiftyfold
+        # (its short LayerNorm kernels wait behind whole-chip GEMM workgroups)
+        for rep in range(2):
+            _corun(chain, enc, load, a, b, c, ref, f"co-run {name} rep {rep}", 50)
     finally:
-        torch.cuda.synchronize()
-        for h in handles:
-            hip.hipStreamDestroy(h)
+        st.close()
+
+
+@pytest.mark.parametrize("name", ["vit22b_tp8"])
+def test_chain_bit_equal_on_cu_masked_streams(name):
+    words = _cu_words()
+    announce(f"CU-masked co-run bit equality {name}")
+    chain, a, b, c = _setup(name)
+    chain.clear()
+    torch.cuda.synchronize()
+    chain.run(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    ref = chain.snapshot()
+    st = MaskedStreams()
+    try:
+        enc_mask = _encoder_mask(words)
+        enc = st.make(enc_mask)
+        load = st.make([(~m) & 0xFFFFFFFF for m in enc_mask])
+        # on disjoint CU sets the chain is slowed only by shared caches and HBM
+        _corun(chain, enc, load, a, b, c, ref, f"masked co-run {name}", 3)
+    finally:
+        st.close()
