@@ -291,6 +291,23 @@ int enc_attn_bwd(int batch, int seq, int heads, int head_dim,
                  const enc_bf16 *do_, enc_bf16 *dqkv, void *ws,
                  size_t ws_bytes, enc_stream_t stream);
 
+/* [For callers that cannot allocate: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.]
+ * enc_attn_bwd without a workspace argument: same kernels, same results, with
+ * the D vector kept in a static device array of the library (4 MiB per GPU,
+ * held until the process ends), so the call allocates nothing and needs no
+ * caller memory beyond its inputs and outputs.  Limit: batch*heads*seq <=
+ * 1048576 (2^20 queries in all), else ENC_ERR_UNSUPPORTED.  The first call
+ * on a device looks the array up for that device (hipGetSymbolAddress); a
+ * failure there is ENC_ERR_LAUNCH.  Every call on one GPU shares that GPU's
+ * array: calls that overlap on one GPU (different streams, or different
+ * threads without ordering) race on it and their results are undefined;
+ * calls ordered on one stream are safe.  Nothing in the array needs to start
+ * at zero (each call writes D before reading it). */
+int enc_attn_bwd_noalloc(int batch, int seq, int heads, int head_dim,
+                         const enc_bf16 *qkv, const enc_bf16 *o, const float *lse,
+                         const enc_bf16 *do_, enc_bf16 *dqkv, enc_stream_t stream);
+
 /* ------------------------------------------------------------ ViT-22B-style block
  *
  * The paper's largest encoder is ViT-22B (Appendix A).  The cited ViT-22B

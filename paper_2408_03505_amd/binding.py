@@ -91,6 +91,7 @@ _SIGS = {
     "enc_qkv_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
     "enc_ln_bwd": [_i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_attn_bwd": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_attn_bwd_noalloc": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p],
     "enc_calib_mfma": [_i, _i, _p, _p],
     "enc_schedule_kernels": [_p, _p, _i, _p, _p, _i, _p, _p],
     "enc_parallel_saved_layout": [_PCFG, ctypes.POINTER(EncPSavedLayout)],
@@ -480,6 +481,22 @@ def enc_attn_bwd(batch, seq, heads, head_dim, qkv, o, lse, do, dqkv=None, ws=Non
         ws = torch.empty(need, dtype=torch.uint8, device=qkv.device)
     _call("enc_attn_bwd", batch, seq, heads, head_dim, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
           _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+    return dqkv
+
+
+def enc_attn_bwd_noalloc(batch, seq, heads, head_dim, qkv, o, lse, do, dqkv, stream=None):
+    """enc_attn_bwd with its D vector in the library's static per-GPU scratch:
+    the C call allocates nothing (dqkv must be given).  Calls that overlap on
+    one GPU race on the scratch."""
+    A = heads * head_dim
+    M = batch * seq
+    _check(qkv, "qkv", (M, 3 * A))
+    _check(o, "o", (M, A))
+    _check(lse, "lse", (batch, heads, seq), torch.float32)
+    _check(do, "do", (M, A))
+    _check(dqkv, "dqkv", (M, 3 * A))
+    _call("enc_attn_bwd_noalloc", batch, seq, heads, head_dim, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
+          _stream(stream))
     return dqkv
 
 

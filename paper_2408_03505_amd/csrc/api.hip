@@ -661,6 +661,27 @@ int enc_attn_bwd(int batch, int seq, int heads, int head_dim, const enc_bf16 *qk
   return launched(fn);
 }
 
+int enc_attn_bwd_noalloc(int batch, int seq, int heads, int head_dim, const enc_bf16 *qkv, const enc_bf16 *o,
+                         const float *lse, const enc_bf16 *do_, enc_bf16 *dqkv, enc_stream_t stream) {
+  const char *fn = "enc_attn_bwd_noalloc";
+  int r = attn_dims(fn, batch, seq, heads, head_dim);
+  if (r) return r;
+  PtrCheck c(fn);
+  c.req(qkv, "qkv").req(o, "o").req(lse, "lse").req(do_, "do").req(dqkv, "dqkv");
+  if (c.code) return c.code;
+  const size_t need = attn_bwd_ws_bytes(batch, seq, heads), have = kAttnScratchFloats * sizeof(float);
+  if (need > have)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: batch*heads*seq = %zu exceeds the static scratch's %zu rows (%zu bytes)", fn,
+                need / sizeof(float), kAttnScratchFloats, have);
+  float *dvec = nullptr;
+  const hipError_t e = attn_bwd_scratch(&dvec);
+  if (e != hipSuccess)
+    return fail(ENC_ERR_LAUNCH, "%s: looking up the static scratch failed: %s", fn, hipGetErrorString(e));
+  if (!launch_attn_bwd(batch, seq, heads, head_dim, qkv, o, lse, do_, dqkv, dvec, as_stream(stream)))
+    return refused_after_checks(fn);
+  return launched(fn);
+}
+
 // ------------------------------------------------------------ composites
 
 int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params, const enc_bf16 *x, enc_bf16 *out, void *saved,

@@ -20,9 +20,20 @@
 // and accumulates dV^T = dO^T P and dK^T = Q^T dS over all queries.
 #include <math.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "lds_dma.hpp"
+
+// Scratch of the allocation-free backward entry point: the D vector
+// (D_i = dO_i . O_i per sequence, head and query, fp32) of calls whose caller
+// cannot allocate a workspace.  Each GPU the library runs on holds its own
+// copy until the process ends.  Host code never passes this name to a kernel
+// (on the host it is a stand-in, not a device address): it uses the address
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[optimus::kAttnScratchFloats];
 
 namespace optimus {
 
@@ -615,6 +626,35 @@ bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf
     case 128: launch_bwd_d<128>(B, S, heads, qkv, o, lse, dO, dqkv, dvec, s); return true;
     default: return false;
   }
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<float *> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t attn_bwd_scratch(float **ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  float *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    // first call on this device: look the array up with the device current
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void *addr = nullptr;
+      e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!addr) return hipErrorInvalidSymbol;
+      p = static_cast<float *>(addr);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return hipSuccess;
 }
 
 }  // namespace optimus

@@ -66,6 +66,11 @@ bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *
 size_t attn_bwd_ws_bytes(int B, int S, int heads);
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s);
+// Static per-device scratch for the allocation-free backward: room for the
+// D vector of B*heads*S <= kAttnScratchFloats queries (4 MiB).  Returns the
+// current device's address of the array (looked up once per device).
+constexpr size_t kAttnScratchFloats = static_cast<size_t>(1) << 20;
+hipError_t attn_bwd_scratch(float **ptr);
 
 // ---- Patch embedding (images -> patch rows; tokens + class token + positions)
 bool launch_patchify(int B, int C, int img_h, int img_w, int p, int Kp, const bf16_t *images, bf16_t *patches,

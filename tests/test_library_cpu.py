@@ -193,6 +193,17 @@ def test_bad_shapes_are_rejected():
 
 
 @no_gpu_only
+def test_noalloc_attention_backward_checks_its_limit():
+    p, z, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0), ctypes.c_void_p(0)
+    # batch*heads*seq past the 2^20 rows of the static scratch
+    assert _status("enc_attn_bwd_noalloc", 256, 257, 16, 64, p, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert b"static scratch" in B.lib().enc_last_error()
+    assert _status("enc_attn_bwd_noalloc", 1, 8, 1, 96, p, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_attn_bwd_noalloc", 1, 8, 1, 64, p, p, p, p, z, s) == B.ENC_ERR_INVALID
+    assert _status("enc_attn_bwd_noalloc", 1, 8, 1, 64, p, p, ctypes.c_void_p(FAKE + 4), p, p, s) == B.ENC_ERR_ALIGN
+
+
+@no_gpu_only
 def test_calibration_arguments_are_checked():
     p, s = ctypes.c_void_p(FAKE), ctypes.c_void_p(0)
     assert _status("enc_calib_mfma", 0, 10, p, s) == B.ENC_ERR_INVALID
