@@ -15,7 +15,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboptimus_enc.so")
+# OPTIMUS_ENC_LIB names another build of the same C ABI (the host-only
+# sanitizer build the CPU tests use); by default the in-tree library loads.
+LIB_PATH = os.environ.get("OPTIMUS_ENC_LIB") or os.path.join(_HERE, "liboptimus_enc.so")
 
 PARAM_ORDER = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
                "ln2_g", "ln2_b", "w_1", "b_1", "w_2", "b_2")

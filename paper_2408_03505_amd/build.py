@@ -1,6 +1,7 @@
 """Build the HIP library liboptimus_enc.so in-tree for gfx950.
 
     python -m paper_2408_03505_amd.build
+    python -m paper_2408_03505_amd.build --host-sanitized   (host-only check build)
 
 Every .hip file under csrc/ is compiled to an object with hipcc and every
 .cpp file (host-only code) with the host C++ compiler, in parallel, and all
@@ -47,6 +48,37 @@ def _compile(src):
     return obj
 
 
+# Host-only build of the C-ABI layer under AddressSanitizer and
+# UndefinedBehaviorSanitizer: api.hip (host code only) and the kernel packer,
+# linked against stand-in launchers (csrc/host_check), with the host compiler
+# alone -- no device code is built or run.  Used by the CPU test suite.
+SAN_DIR = os.path.join(OBJ, "host_san")
+SAN_LIB = os.path.join(SAN_DIR, "liboptimus_enc_host_san.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g", "-O1"]
+
+
+def build_host_sanitized(verbose=True):
+    os.makedirs(SAN_DIR, exist_ok=True)
+    srcs = [(os.path.join(CSRC, "api.hip"), ["-x", "c++"]),
+            (os.path.join(CSRC, "scheduler.cpp"), []),
+            (os.path.join(CSRC, "host_check", "stub_launchers.cpp"), [])]
+    inc = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", f"-I{os.path.join(ROOT, 'include')}"]
+    objs = []
+    for src, lang in srcs:
+        obj = os.path.join(SAN_DIR, os.path.basename(src) + ".o")
+        cmd = [CXX, *lang, "-std=c++17", "-fPIC", "-Wall", *inc, *SAN_FLAGS, "-c", src, "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"compiling {src} failed:\n{r.stdout}\n{r.stderr}")
+        objs.append(obj)
+    r = subprocess.run([CXX, "-shared", *SAN_FLAGS, "-o", SAN_LIB, *objs], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
 def build(verbose=True):
     os.makedirs(OBJ, exist_ok=True)
     srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
@@ -64,5 +96,8 @@ def build(verbose=True):
 
 
 if __name__ == "__main__":
-    build()
+    if "--host-sanitized" in sys.argv[1:]:
+        build_host_sanitized()
+    else:
+        build()
     sys.exit(0)

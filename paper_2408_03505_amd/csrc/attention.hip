@@ -600,10 +600,6 @@ void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, c
 
 }  // namespace
 
-size_t attn_bwd_ws_bytes(int B, int S, int heads) {
-  return static_cast<size_t>(B) * heads * S * sizeof(float);
-}
-
 bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
   // every tile address (up to one tile past the tensor) must stay a 32-bit buffer offset
   const uint64_t ld = 3ull * heads * d;

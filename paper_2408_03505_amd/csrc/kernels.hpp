@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "geometry.hpp"
+
 namespace optimus {
 
 typedef uint16_t bf16_t;
@@ -14,7 +16,6 @@ typedef uint16_t bf16_t;
 // ---- LayerNorm
 bool launch_ln_fwd(int rows, int cols, const bf16_t *x, const bf16_t *gamma, const bf16_t *beta, float eps,
                    bf16_t *y, float *mean, float *rstd, hipStream_t s);
-size_t ln_bwd_ws_bytes(int rows, int cols);
 bool launch_ln_bwd(int rows, int cols, const bf16_t *dy, const bf16_t *x, const float *mean, const float *rstd,
                    const bf16_t *gamma, const bf16_t *dresid, bf16_t *dx, float *dgamma, float *dbeta,
                    int accumulate, float *part, hipStream_t s);
@@ -56,14 +57,12 @@ bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s);
 // ---- QK normalisation (LayerNorm of every query and key vector over head_dim)
 bool launch_qk_norm_fwd(int M, int heads, int d, const bf16_t *qkv, const bf16_t *qg, const bf16_t *qb,
                         const bf16_t *kg, const bf16_t *kb, float eps, bf16_t *qkvn, float *stats, hipStream_t s);
-size_t qk_norm_bwd_ws_bytes(int M, int heads, int d);
 bool launch_qk_norm_bwd(int M, int heads, int d, const bf16_t *dqkvn, const bf16_t *qkv, const float *stats,
                         const bf16_t *qg, const bf16_t *kg, bf16_t *dqkv, float *dqg, float *dqb, float *dkg,
                         float *dkb, int accumulate, float *part, hipStream_t s);
 
 // ---- Attention
 bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s);
-size_t attn_bwd_ws_bytes(int B, int S, int heads);
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s);
 // Static per-device scratch for the allocation-free backward: room for the

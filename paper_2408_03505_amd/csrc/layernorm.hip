@@ -16,7 +16,7 @@ namespace optimus {
 
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = kLnThreads;
 
 // Sum over the TPR threads that share a row (TPR = 64 or 256).
 template <int TPR, int NV>
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(int rows, int cols, co
 // Blocks (partial rows) of the backward pass: one per CU.  Measured at
 // 2048 x 6144: 512, 1024 and 2048 blocks are slower (the partials grow with
 // the block count), and so is loading two rows ahead instead of one.
-constexpr int kBwdBlocks = 256;
+constexpr int kBwdBlocks = kLnBwdBlocks;
 
 template <int TPR, int CPT, bool RES>
 __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(int rows, int cols, int rows_per_block,
@@ -359,28 +359,7 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_reduce_kernel(int nblk, int c
   }
 }
 
-// Threads per row of the backward pass: one wave up to 2048 columns (four
-// rows in flight per 256-thread block), the whole block beyond.
-int bwd_tpr(int cols) { return (cols >> 3) > 256 ? 256 : 64; }
-
-// Rows per block of the backward pass (a multiple of the rows in flight).
-int bwd_rows_per_block(int rows, int cols) {
-  const int rg = kThreads / bwd_tpr(cols);
-  int rpb = (rows + kBwdBlocks - 1) / kBwdBlocks;
-  rpb = (rpb + rg - 1) / rg * rg;
-  return rpb < rg ? rg : rpb;
-}
-
-int bwd_blocks(int rows, int cols) {
-  const int rpb = bwd_rows_per_block(rows, cols);
-  return (rows + rpb - 1) / rpb;
-}
-
 }  // namespace
-
-size_t ln_bwd_ws_bytes(int rows, int cols) {
-  return static_cast<size_t>(bwd_blocks(rows, cols)) * static_cast<size_t>(cols) * 2 * sizeof(float);
-}
 
 #define OPT_LN_DISPATCH(KERNEL, ...)                                                                           \
   do {                                                                                                          \
@@ -417,8 +396,8 @@ bool launch_ln_bwd(int rows, int cols, const bf16_t *dy, const bf16_t *x, const 
                    const bf16_t *gamma, const bf16_t *dresid, bf16_t *dx, float *dgamma, float *dbeta,
                    int accumulate, float *part, hipStream_t s) {
   const int nch = cols >> 3;
-  const int tpr = bwd_tpr(cols);
-  const int rpb = bwd_rows_per_block(rows, cols);
+  const int tpr = ln_bwd_tpr(cols);
+  const int rpb = ln_bwd_rows_per_block(rows, cols);
   const int nblk = (rows + rpb - 1) / rpb;
   const dim3 grid(nblk);
   // LDS for the hand-over of column sums between the row groups of a block

@@ -19,7 +19,7 @@ namespace optimus {
 
 namespace {
 
-constexpr int kGroups = 16;  // 16-lane groups per 256-thread block
+constexpr int kGroups = kQkGroups;  // 16-lane groups per 256-thread block
 
 __device__ __forceinline__ float group16_sum(float v) {
 #pragma unroll
@@ -184,12 +184,6 @@ __global__ __launch_bounds__(256) void qk_norm_reduce_kernel(int blocks, int D, 
   }
 }
 
-int bwd_blocks(int M, int heads) {
-  const long pairs = static_cast<long>(M) * heads;
-  const long want = (pairs + kGroups - 1) / kGroups;
-  return static_cast<int>(want < 1024 ? want : 1024);
-}
-
 template <int D>
 void fwd_d(int M, int heads, const bf16_t *qkv, const bf16_t *qg, const bf16_t *qb, const bf16_t *kg,
            const bf16_t *kb, float eps, bf16_t *qkvn, float *stats, hipStream_t s) {
@@ -202,7 +196,7 @@ template <int D>
 void bwd_d(int M, int heads, const bf16_t *dqkvn, const bf16_t *qkv, const float *stats, const bf16_t *qg,
            const bf16_t *kg, bf16_t *dqkv, float *dqg, float *dqb, float *dkg, float *dkb, int accumulate,
            float *part, hipStream_t s) {
-  const int nb = bwd_blocks(M, heads);
+  const int nb = qk_norm_bwd_blocks(M, heads);
   hipLaunchKernelGGL(qk_norm_bwd_kernel<D>, dim3(nb), dim3(256), 0, s, M * heads, heads, dqkvn, qkv, stats, qg, kg,
                      dqkv, part);
   hipLaunchKernelGGL(qk_norm_reduce_kernel, dim3(4 * D), dim3(256), 0, s, nb, D, part, dqg, dqb, dkg, dkb,
@@ -219,10 +213,6 @@ bool launch_qk_norm_fwd(int M, int heads, int d, const bf16_t *qkv, const bf16_t
     case 128: fwd_d<128>(M, heads, qkv, qg, qb, kg, kb, eps, qkvn, stats, s); return true;
     default: return false;
   }
-}
-
-size_t qk_norm_bwd_ws_bytes(int M, int heads, int d) {
-  return static_cast<size_t>(bwd_blocks(M, heads)) * 4 * d * sizeof(float);
 }
 
 bool launch_qk_norm_bwd(int M, int heads, int d, const bf16_t *dqkvn, const bf16_t *qkv, const float *stats,
