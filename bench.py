@@ -16,6 +16,7 @@ bounded sample of the same workload.
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -804,18 +805,30 @@ def step_flops(cfg):
     return sum(f for f, _ in kernel_work(cfg).values())
 
 
-def cpu_baseline(cfg, x, params, dout, budget_s):
-    """The float64 oracle's layer forward+backward on whole sequences of the
-    same workload (as many as fit the time budget, at least one)."""
-    import oracle
-    from threadpoolctl import threadpool_info
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.lower().startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
 
-    S, H = cfg["seq"], cfg["hidden"]
+
+def _oracle_seconds(cfg, x, params, dout, budget_s, max_seqs=None):
+    """Time the float64 oracle's forward+backward on whole sequences of cfg,
+    one after another, until the budget would be exceeded (at least one).
+    Returns (flops, seconds, sequences)."""
+    import oracle
+
+    S = cfg["seq"]
     p64 = {n: params[n].to(torch.float64).numpy() for n in params}
-    done, t_used, flops = 0, 0.0, 0
     one = dict(cfg, batch=1)
     f1 = 3 * oracle.layer_flops(one)
-    while done < cfg["batch"]:
+    limit = cfg["batch"] if max_seqs is None else min(cfg["batch"], max_seqs)
+    done, t_used = 0, 0.0
+    while done < limit:
         xs = x[done * S:(done + 1) * S].to(torch.float64).numpy()
         ds = dout[done * S:(done + 1) * S].to(torch.float64).numpy()
         t0 = time.perf_counter()
@@ -823,14 +836,51 @@ def cpu_baseline(cfg, x, params, dout, budget_s):
         oracle.layer_bwd(one, p64, xs, saved, ds)
         t_used += time.perf_counter() - t0
         done += 1
-        flops += f1
         if t_used + t_used / done > budget_s:
             break
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": flops / t_used / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 oracle forward+backward of {done} of {cfg['batch']} sequences "
-                      f"({done * S} tokens) of the same layer, {t_used:.1f} s",
-            "host_cpus": len(os.sched_getaffinity(0))}
+    return f1 * done, t_used, done
+
+
+def cpu_baseline(cfg, x, params, dout, budget_s, name=None, seed=0, configs=None):
+    """The float64 oracle (numpy with the host BLAS's threads for matmul,
+    scipy for erf; as it stands, not tuned) timed on the host cores: the
+    headline on whole sequences of the benchmarked workload within the time
+    budget; one sequence of every other workload with all threads; and one
+    sequence of the three ViT-sized workloads on a single thread."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs
+
+    flops, secs, done = _oracle_seconds(cfg, x, params, dout, budget_s)
+    pools = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in pools] or [1])
+    res = {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"float64 oracle forward+backward of {done} of {cfg['batch']} sequences "
+                     f"({done * cfg['seq']} tokens) of the same layer, {secs:.1f} s",
+           "oracle": "float64 numpy: BLAS matmul on the host's threads, scipy erf, everything else numpy",
+           "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0)),
+           "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+           "blas": [{k: i.get(k) for k in ("internal_api", "version", "num_threads", "threading_layer")}
+                    for i in pools]}
+    per, single = {}, {}
+    for cname in (configs if configs is not None else CONFIGS):
+        ccfg = CONFIGS[cname]
+        if cname == name:
+            cx, cp, cd = x, params, dout
+        else:
+            cx, cp, cd = layer_inputs(ccfg, seed=seed)
+        f, t, n = _oracle_seconds(ccfg, cx, cp, cd, budget_s=0.0, max_seqs=1)
+        per[cname] = {"tflops": round(f / t / 1e12, 4), "s_per_sequence": round(t / n, 4),
+                      "sample": f"{n} of {ccfg['batch']} sequences"}
+        if cname in ("vit_tiny", "vit_base", "vit_huge"):
+            with threadpool_limits(limits=1):
+                f, t, n = _oracle_seconds(ccfg, cx, cp, cd, budget_s=0.0, max_seqs=1)
+            single[cname] = {"tflops": round(f / t / 1e12, 4), "s_per_sequence": round(t / n, 4),
+                             "sample": f"{n} of {ccfg['batch']} sequences, 1 thread"}
+        del cx, cp, cd
+    res["per_config"] = per
+    res["single_thread"] = single
+    return res
 
 
 def main():
@@ -1000,7 +1050,7 @@ def main():
         torch.cuda.synchronize()
         res["copy_reference_bytes"] = args.copy_mib << 20
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, x, params, dout, args.cpu_budget_s)
+        res["cpu_baseline"] = cpu_baseline(cfg, x, params, dout, args.cpu_budget_s, args.config, args.seed)
     print(json.dumps(res), flush=True)
 
 

@@ -161,3 +161,15 @@ def test_pmc_summary_per_entry_and_busy_fraction(tmp_path):
         u = bench.pmc_utilisation(ent[n])
         assert u["mfma_busy"] == pytest.approx(0.5)
         assert u["wait_any_per_wave_cycle"] == pytest.approx(0.3)
+
+
+def test_cpu_baseline_reports_host_and_per_config_figures():
+    from paper_2408_03505_amd.synthetic import CONFIGS, layer_inputs
+    cfg = CONFIGS["vit_tiny"]
+    x, params, dout = layer_inputs(cfg, seed=0)
+    r = bench.cpu_baseline(cfg, x, params, dout, budget_s=0.5, name="vit_tiny", configs=["vit_tiny", "vit_base"])
+    assert r["kind"] == "oracle" and r["value"] > 0 and r["cores"] >= 1
+    assert r["cpu_model"] and r["host_cpus"] >= 1 and "float64" in r["oracle"]
+    assert set(r["per_config"]) == {"vit_tiny", "vit_base"} and set(r["single_thread"]) == {"vit_tiny", "vit_base"}
+    for v in list(r["per_config"].values()) + list(r["single_thread"].values()):
+        assert v["tflops"] > 0 and v["s_per_sequence"] > 0
