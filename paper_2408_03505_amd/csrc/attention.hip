@@ -20,6 +20,7 @@
 // and accumulates dV^T = dO^T P and dK^T = Q^T dS over all queries.
 #include <math.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -39,8 +40,7 @@ namespace optimus {
 
 namespace {
 
-constexpr int kKT = 64;     // keys (forward, dQ) or queries (dK/dV) per LDS tile
-constexpr int kRows = 128;  // queries (or keys) per workgroup: 4 waves x 32
+constexpr int kRows = 128;  // queries per forward workgroup: 4 waves x 32
 constexpr float kLog2e = 1.4426950408889634f;
 
 // 2^x on the hardware exponential (v_exp_f32).  Every argument here is a
@@ -137,47 +137,73 @@ __device__ __forceinline__ void store_dmajor_lds(bf16_t *dst, size_t ld, const f
 // ds_read_b128 pattern) and spreading any 4 consecutive rows over disjoint
 // 64-byte ranges (the transpose-read pattern).
 
-constexpr int kDL = 128;                    // LDS row length (elements)
-constexpr int kTileBytes = kKT * kDL * 2;   // one 64-token tile: 16 KB
+constexpr int kDL = 128;  // LDS row length (elements)
+constexpr int kMaxKT = 64;  // longest token tile of any kernel (bounds the DMA overhang past a tensor)
+
+// Bytes of one tile of KT tokens (KT = 32: 8 KB; KT = 64: 16 KB).
+template <int KT>
+constexpr int tile_bytes() {
+  return KT * kDL * 2;
+}
 
 __device__ __forceinline__ int tsw(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 __device__ __forceinline__ int tile_off(int r, int c) { return r * (kDL * 2) + ((c ^ tsw(r)) << 4); }
 __device__ __forceinline__ int perm23(int r) { return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
-// Per-lane byte offsets of this wave's DMA loads of one tile (16 loads of
+// Per-lane byte offsets of this wave's DMA loads of one tile (KT/4 loads of
 // 1 KB per tile, split over NW waves; tile-relative: the tile's first row and
 // column go in the scalar offset).  perm stores token perm23(r) in row r.
-template <int NW>
-__device__ __forceinline__ void tile_voff(uint32_t (&v)[16 / NW], int wid, int lane, int ld, bool perm) {
+template <int KT, int NW>
+struct TileLoads {
+  static constexpr int N = KT / 4 / NW;  // 1 KB loads per wave per tile
+  static_assert(N >= 1 && N * NW * 4 == KT, "tile rows must split evenly over the waves");
+};
+
+template <int KT, int NW, int N>
+__device__ __forceinline__ void tile_voff(uint32_t (&v)[N], int wid, int lane, int ld, bool perm) {
+  static_assert(N == TileLoads<KT, NW>::N, "one offset per load");
 #pragma unroll
-  for (int i = 0; i < 16 / NW; ++i) {
-    const int o = (wid * (16 / NW) + i) * 1024 + lane * 16;
+  for (int i = 0; i < N; ++i) {
+    const int o = (wid * N + i) * 1024 + lane * 16;
     const int pr = o >> 8, c = ((o & 255) >> 4) ^ tsw(pr);
     v[i] = static_cast<uint32_t>(((perm ? perm23(pr) : pr) * ld + c * 8) * 2);
   }
 }
 
-// Issue one tile's DMA loads.  In the last tile of a sequence (rem < kKT
+// Issue one tile's DMA loads.  In the last tile of a sequence (rem < KT
 // rows left) the rows past the sequence re-read the tile's first row: every
 // product with those rows carries a zero weight, but a non-finite value in
 // the next sequence would still turn that zero into NaN.
-template <int NW>
-__device__ __forceinline__ void tile_issue(const u32x4_t &rsrc, uint32_t lds_tile, const uint32_t (&voff)[16 / NW],
+template <int KT, int NW, int N>
+__device__ __forceinline__ void tile_issue(const u32x4_t &rsrc, uint32_t lds_tile, const uint32_t (&voff)[N],
                                            uint32_t soff, int wid, int lane, int rem, int ld, bool perm) {
+  static_assert(N == TileLoads<KT, NW>::N, "one offset per load");
   const uint32_t sl = __builtin_amdgcn_readfirstlane(soff);
-  if (rem >= kKT) {
+  if (rem >= KT) {
 #pragma unroll
-    for (int i = 0; i < 16 / NW; ++i)
-      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * (16 / NW) + i) * 1024), voff[i], sl);
+    for (int i = 0; i < N; ++i)
+      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * N + i) * 1024), voff[i], sl);
   } else {
 #pragma unroll
-    for (int i = 0; i < 16 / NW; ++i) {
-      const int pr = (wid * (16 / NW) + i) * 4 + (lane >> 4);
+    for (int i = 0; i < N; ++i) {
+      const int pr = (wid * N + i) * 4 + (lane >> 4);
       const int tok = perm ? perm23(pr) : pr;
       const uint32_t v = tok < rem ? voff[i] : voff[i] - static_cast<uint32_t>(tok * ld * 2);
-      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * (16 / NW) + i) * 1024), v, sl);
+      buffer_load_lds16(rsrc, __builtin_amdgcn_readfirstlane(lds_tile + (wid * N + i) * 1024), v, sl);
     }
   }
+}
+
+// Wait for the oldest tile in flight: with `ahead` later tiles already issued
+// (each L loads per wave) those may stay outstanding.
+template <int L>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if (ahead >= 2)
+    wait_vmcnt<2 * L>();
+  else if (ahead == 1)
+    wait_vmcnt<L>();
+  else
+    wait_vmcnt<0>();
 }
 
 __device__ __forceinline__ void block_barrier() {
@@ -215,12 +241,14 @@ __device__ __forceinline__ bf16x8_t tile_cols_perm(const lds_char *t, int nbase,
   return lds_read_tr(t + tile_off(k, n >> 3) + in, t + tile_off(k + 8, n >> 3) + in);
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
-                                                       uint32_t qkv_bytes, bf16_t *__restrict__ o,
-                                                       float *__restrict__ lse) {
+template <int D, int KT, int ST, int MINB>
+__global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
+                                                          uint32_t qkv_bytes, bf16_t *__restrict__ o,
+                                                          float *__restrict__ lse) {
   using H = Head<D>;
-  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];  // 2 x (K tile, V tile)
+  constexpr int TB = tile_bytes<KT>(), NL = TileLoads<KT, 4>::N;
+  static_assert(ST == 2 || ST == 3, "two or three tile stages");
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];  // ST x (K tile, V tile)
   const lds_char *smem = (const lds_char *)(smem_raw);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
@@ -233,20 +261,21 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q = qt * kRows + wid * 32 + (lane & 31);
   const bool qvalid = q < S;
+  const bool active = qt * kRows + wid * 32 < S;  // wave-uniform
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
 
   const u32x4_t rsrc = make_rsrc(qkv, qkv_bytes);
-  uint32_t voff_k[4], voff_v[4];
-  tile_voff<4>(voff_k, wid, lane, ld, false);
-  tile_voff<4>(voff_v, wid, lane, ld, true);
+  uint32_t voff_k[NL], voff_v[NL];
+  tile_voff<KT, 4>(voff_k, wid, lane, ld, false);
+  tile_voff<KT, 4>(voff_v, wid, lane, ld, true);
   const uint32_t k_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + A + h * D) * 2);
   const uint32_t v_base = k_base + static_cast<uint32_t>(A * 2);
-  const uint32_t tile_step = static_cast<uint32_t>(kKT * ld * 2);
+  const uint32_t tile_step = static_cast<uint32_t>(KT * ld * 2);
   auto issue = [&](int t) {
-    const uint32_t buf = lds0 + (t & 1) * 2 * kTileBytes;
-    const int rem = S - t * kKT;
-    tile_issue<4>(rsrc, buf, voff_k, k_base + t * tile_step, wid, lane, rem, ld, false);
-    tile_issue<4>(rsrc, buf + kTileBytes, voff_v, v_base + t * tile_step, wid, lane, rem, ld, true);
+    const uint32_t buf = lds0 + (t % ST) * 2 * TB;
+    const int rem = S - t * KT;
+    tile_issue<KT, 4>(rsrc, buf, voff_k, k_base + t * tile_step, wid, lane, rem, ld, false);
+    tile_issue<KT, 4>(rsrc, buf + TB, voff_v, v_base + t * tile_step, wid, lane, rem, ld, true);
   };
 
   bf16x8_t qf[H::KS];
@@ -258,30 +287,28 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
   float m = -INFINITY, l = 0.f;
   const float c = kLog2e / sqrtf(static_cast<float>(D));
 
-  const int nk = (S + kKT - 1) / kKT;
-  issue(0);
+  const int nk = (S + KT - 1) / KT;
+  for (int t = 0; t < ST - 1 && t < nk; ++t) issue(t);
   for (int t = 0; t < nk; ++t) {
-    if (t + 1 < nk) {
-      issue(t + 1);
-      wait_vmcnt<8>();  // this wave's 8 loads of tile t+1 may stay in flight
-    } else {
-      wait_vmcnt<0>();
-    }
+    if (t + ST - 1 < nk) issue(t + ST - 1);
+    // this wave's loads of the later tiles already issued may stay in flight
+    wait_tiles<2 * NL>(min(nk - 1 - t, ST - 1));
     block_barrier();
-    const lds_char *Ks = smem + (t & 1) * 2 * kTileBytes;
-    const lds_char *Vs = Ks + kTileBytes;
-    const int k0 = t * kKT;
-
-    f32x16_t s[2];
+    const lds_char *Ks = smem + (t % ST) * 2 * TB;
+    const lds_char *Vs = Ks + TB;
+    const int k0 = t * KT;
+    if (active) {  // waves whose queries all lie past the sequence only load and synchronise
+    constexpr int NS = KT / 32;  // 32-key fragments per tile
+    f32x16_t s[NS];
 #pragma unroll
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NS; ++f) {
       s[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) s[f] = mfma32(tile_rows(Ks, f * 32, kk, lane), qf[kk], s[f]);
     }
     float mt = m;
 #pragma unroll
-    for (int f = 0; f < 2; ++f)
+    for (int f = 0; f < NS; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
@@ -294,7 +321,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
     m = mt;
     float ls = 0.f;
 #pragma unroll
-    for (int f = 0; f < 2; ++f)
+    for (int f = 0; f < NS; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float pv = exp2_hw(s[f][i] - mt);
@@ -305,10 +332,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
 #pragma unroll
     for (int nf = 0; nf < H::NF; ++nf) acc[nf] *= alpha;
 #pragma unroll
-    for (int st = 0; st < kKT / 16; ++st) {
+    for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t pb = pack8(s[st >> 1], st & 1);
 #pragma unroll
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Vs, nf * 32, st, lane), pb, acc[nf]);
+    }
     }
     block_barrier();  // every wave is done with this buffer before it is refilled
   }
@@ -328,14 +356,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(int B, int S, int head
 // permuted transpose read, which matches the token order of the dS^T
 // registers.  This kernel also writes D_i = dO_i . O_i for the dK/dV kernel.
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
-                                                              uint32_t qkv_bytes, const bf16_t *__restrict__ o,
-                                                              const float *__restrict__ lse,
-                                                              const bf16_t *__restrict__ dO, bf16_t *__restrict__ dqkv,
-                                                              float *__restrict__ dvec) {
+template <int D, int NW, int KT, int ST, int MINB>
+__global__ __launch_bounds__(NW * 64, MINB) void attn_bwd_dq_kernel(int B, int S, int heads,
+                                                                    const bf16_t *__restrict__ qkv, uint32_t qkv_bytes,
+                                                                    const bf16_t *__restrict__ o,
+                                                                    const float *__restrict__ lse,
+                                                                    const bf16_t *__restrict__ dO,
+                                                                    bf16_t *__restrict__ dqkv, float *__restrict__ dvec) {
   using H = Head<D>;
-  constexpr int ROWS = 32 * NW, STAGE = 2 * kTileBytes;  // K, V
+  constexpr int TB = tile_bytes<KT>(), NL = TileLoads<KT, NW>::N;
+  constexpr int ROWS = 32 * NW, STAGE = 2 * TB;  // K, V
+  static_assert(ST == 2 || ST == 3, "two or three tile stages");
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
   const lds_char *smem = (const lds_char *)(smem_raw);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
@@ -349,20 +380,21 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q = qt * ROWS + wid * 32 + (lane & 31);
   const bool qvalid = q < S;
+  const bool active = qt * ROWS + wid * 32 < S;  // wave-uniform
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
   const size_t orow = (static_cast<size_t>(b) * S + q) * A + h * D;
 
   const u32x4_t rsrc = make_rsrc(qkv, qkv_bytes);
-  uint32_t voff[16 / NW];
-  tile_voff<NW>(voff, wid, lane, ld, false);
+  uint32_t voff[NL];
+  tile_voff<KT, NW>(voff, wid, lane, ld, false);
   const uint32_t k_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + A + h * D) * 2);
   const uint32_t v_base = k_base + static_cast<uint32_t>(A * 2);
-  const uint32_t tile_step = static_cast<uint32_t>(kKT * ld * 2);
+  const uint32_t tile_step = static_cast<uint32_t>(KT * ld * 2);
   auto issue = [&](int t) {
-    const uint32_t buf = lds0 + (t & 1) * STAGE;
-    const int rem = S - t * kKT;
-    tile_issue<NW>(rsrc, buf, voff, k_base + t * tile_step, wid, lane, rem, ld, false);
-    tile_issue<NW>(rsrc, buf + kTileBytes, voff, v_base + t * tile_step, wid, lane, rem, ld, false);
+    const uint32_t buf = lds0 + (t % ST) * STAGE;
+    const int rem = S - t * KT;
+    tile_issue<KT, NW>(rsrc, buf, voff, k_base + t * tile_step, wid, lane, rem, ld, false);
+    tile_issue<KT, NW>(rsrc, buf + TB, voff, v_base + t * tile_step, wid, lane, rem, ld, false);
   };
 
   bf16x8_t qf[H::KS], df[H::KS];
@@ -386,22 +418,20 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
   f32x16_t acc[H::NF];
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
-  constexpr int LOADS = 2 * (16 / NW);
-  const int nk = (S + kKT - 1) / kKT;
-  issue(0);
+  constexpr int LOADS = 2 * NL;
+  constexpr int NS = KT / 32;  // 32-key fragments per tile
+  const int nk = (S + KT - 1) / KT;
+  for (int t = 0; t < ST - 1 && t < nk; ++t) issue(t);
   for (int t = 0; t < nk; ++t) {
-    if (t + 1 < nk) {
-      issue(t + 1);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    if (t + ST - 1 < nk) issue(t + ST - 1);
+    wait_tiles<LOADS>(min(nk - 1 - t, ST - 1));
     block_barrier();
-    const lds_char *Ks = smem + (t & 1) * STAGE, *Vs = Ks + kTileBytes;
-    const int k0 = t * kKT;
-    f32x16_t sv[2], dp[2];
+    const lds_char *Ks = smem + (t % ST) * STAGE, *Vs = Ks + TB;
+    const int k0 = t * KT;
+    if (active) {  // waves whose queries all lie past the sequence only load and synchronise
+    f32x16_t sv[NS], dp[NS];
 #pragma unroll
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NS; ++f) {
       sv[f] = f32x16_t{};
       dp[f] = f32x16_t{};
 #pragma unroll
@@ -412,17 +442,18 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
     }
     // register i of fragment f is key k0 + f*32 + 8(i/4) + 4 hf + i%4
 #pragma unroll
-    for (int f = 0; f < 2; ++f)
+    for (int f = 0; f < NS; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
         sv[f][i] = (key < S) ? exp2_hw(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
       }
 #pragma unroll
-    for (int st = 0; st < kKT / 16; ++st) {
+    for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t sb = pack8(sv[st >> 1], st & 1);
 #pragma unroll
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Ks, nf * 32, st, lane), sb, acc[nf]);
+    }
     }
     block_barrier();
   }
@@ -444,17 +475,27 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(int B, int S, int 
 // the dV and dK products with the permuted transpose read.  lse and D of the
 // tile's queries come in by DMA; queries past the sequence are masked out.
 
-template <int D, int NG>
-__global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, int heads,
-                                                                 const bf16_t *__restrict__ qkv, uint32_t qkv_bytes,
-                                                                 const float *__restrict__ lse,
-                                                                 const bf16_t *__restrict__ dO, uint32_t do_bytes,
-                                                                 const float *__restrict__ dvec,
-                                                                 bf16_t *__restrict__ dqkv) {
+// LDS of one dK/dV stage: the Q and dO tiles, then lse and D of up to 64
+// queries each (a 64-lane DMA; entries past the tile are never read).
+template <int KT>
+constexpr int dkdv_stage_bytes() {
+  return 2 * tile_bytes<KT>() + 2 * 64 * 4;
+}
+
+template <int D, int NG, int KT, int MINB>
+__global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, int S, int heads,
+                                                                       const bf16_t *__restrict__ qkv,
+                                                                       uint32_t qkv_bytes,
+                                                                       const float *__restrict__ lse,
+                                                                       const bf16_t *__restrict__ dO,
+                                                                       uint32_t do_bytes,
+                                                                       const float *__restrict__ dvec,
+                                                                       bf16_t *__restrict__ dqkv) {
   using H = Head<D>;
-  constexpr int NW = 2 * NG, ROWS = 32 * NG, TILES = 2 * kTileBytes;  // Q, dO
-  constexpr int STAGE = TILES + 2 * kKT * 4;                           // + lse, D
-  constexpr int PX = 2 * STAGE;  // P hand-over: one 8 KB slot per key group
+  constexpr int TB = tile_bytes<KT>(), NL = TileLoads<KT, 2 * NG>::N;
+  constexpr int NW = 2 * NG, ROWS = 32 * NG, TILES = 2 * TB;  // Q, dO
+  constexpr int STAGE = dkdv_stage_bytes<KT>();                // + lse, D
+  constexpr int PX = 2 * STAGE;  // P hand-over: one 32 x KT fp32 slot per key group
   extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
   const lds_char *smem = (const lds_char *)(smem_raw);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
@@ -469,29 +510,30 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
   const bool role_a = wid < NG;  // wave-uniform
   const int grp = role_a ? wid : wid - NG;
   const int k0w = kt * ROWS + grp * 32;
+  const bool active = k0w < S;  // wave-uniform
   const int key = k0w + (lane & 31);
   const bool kvalid = key < S;
   const bf16_t *base = qkv + static_cast<size_t>(b) * S * ld;
 
   const u32x4_t rq = make_rsrc(qkv, qkv_bytes), rd = make_rsrc(dO, do_bytes);
-  uint32_t vq[16 / NW], vd[16 / NW];
-  tile_voff<NW>(vq, wid, lane, ld, false);
-  tile_voff<NW>(vd, wid, lane, A, false);
+  uint32_t vq[NL], vd[NL];
+  tile_voff<KT, NW>(vq, wid, lane, ld, false);
+  tile_voff<KT, NW>(vd, wid, lane, A, false);
   const uint32_t q_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * ld + h * D) * 2);
   const uint32_t d_base = static_cast<uint32_t>((static_cast<size_t>(b) * S * A + h * D) * 2);
-  const uint32_t q_step = static_cast<uint32_t>(kKT * ld * 2), d_step = static_cast<uint32_t>(kKT * A * 2);
+  const uint32_t q_step = static_cast<uint32_t>(KT * ld * 2), d_step = static_cast<uint32_t>(KT * A * 2);
   const uint32_t vec_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * heads * S * 4);
   const u32x4_t rl = make_rsrc(lse, vec_bytes), rv = make_rsrc(dvec, vec_bytes);
   auto issue = [&](int t) {
     const uint32_t buf = lds0 + (t & 1) * STAGE;
-    const int rem = S - t * kKT;
-    tile_issue<NW>(rq, buf, vq, q_base + t * q_step, wid, lane, rem, ld, false);
-    tile_issue<NW>(rd, buf + kTileBytes, vd, d_base + t * d_step, wid, lane, rem, A, false);
-    // lse (wave 0) and D (wave 1) of the tile's 64 queries; entries past the
-    // sequence are masked out of P below
-    const uint32_t vs = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((bh * S + t * kKT) * 4));
+    const int rem = S - t * KT;
+    tile_issue<KT, NW>(rq, buf, vq, q_base + t * q_step, wid, lane, rem, ld, false);
+    tile_issue<KT, NW>(rd, buf + TB, vd, d_base + t * d_step, wid, lane, rem, A, false);
+    // lse (wave 0) and D (wave 1) of 64 queries from the tile's first; entries
+    // past the tile or the sequence are never used (masked out of P below)
+    const uint32_t vs = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((bh * S + t * KT) * 4));
     if (wid == 0) buffer_load_lds4(rl, __builtin_amdgcn_readfirstlane(buf + TILES), lane * 4, vs);
-    if (wid == 1) buffer_load_lds4(rv, __builtin_amdgcn_readfirstlane(buf + TILES + kKT * 4), lane * 4, vs);
+    if (wid == 1) buffer_load_lds4(rv, __builtin_amdgcn_readfirstlane(buf + TILES + 64 * 4), lane * 4, vs);
   };
 
   // K rows (wave A) or V rows (wave B) of this lane's key
@@ -501,10 +543,11 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
   f32x16_t acc[H::NF];  // dV^T (wave A) or dK^T (wave B)
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
-  float *px = reinterpret_cast<float *>(smem_raw + PX) + grp * (32 * 64);
+  float *px = reinterpret_cast<float *>(smem_raw + PX) + grp * (32 * KT);
   const float c = kLog2e / sqrtf(static_cast<float>(D));
-  constexpr int LOADS = 2 * (16 / NW);
-  const int nq = (S + kKT - 1) / kKT;
+  constexpr int LOADS = 2 * NL;
+  constexpr int NS = KT / 32;  // 32-query fragments per tile
+  const int nq = (S + KT - 1) / KT;
   issue(0);
   for (int t = 0; t < nq; ++t) {
     if (t + 1 < nq) {
@@ -517,22 +560,25 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
       wait_vmcnt<0>();
     }
     block_barrier();
-    const lds_char *Qs = smem + (t & 1) * STAGE, *Ds = Qs + kTileBytes;
+    const lds_char *Qs = smem + (t & 1) * STAGE, *Ds = Qs + TB;
     const float *Ls = reinterpret_cast<const float *>(smem_raw + (t & 1) * STAGE + TILES);
-    const int q0 = t * kKT;
+    const int q0 = t * KT;
     // S^T (wave A) or dP^T (wave B): register 4g+e of fragment f is query
     // f*32 + 8g + 4hf + e (four consecutive queries)
     const lds_char *Rs = role_a ? Qs : Ds;
-    f32x16_t sv[2];
+    f32x16_t sv[NS];
+    // waves whose keys all lie past the sequence only load and synchronise
+    // (both waves of a key group agree)
+    if (active) {
 #pragma unroll
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NS; ++f) {
       sv[f] = f32x16_t{};
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) sv[f] = mfma32(tile_rows(Rs, f * 32, kk, lane), rf[kk], sv[f]);
     }
     if (role_a) {
 #pragma unroll
-      for (int f = 0; f < 2; ++f)
+      for (int f = 0; f < NS; ++f)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int qi = f * 32 + 8 * g + 4 * hf;
@@ -545,14 +591,16 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
           }
         }
     }
+    }
     lds_barrier();  // P of every group is in LDS
+    if (active) {
     if (!role_a) {
 #pragma unroll
-      for (int f = 0; f < 2; ++f)
+      for (int f = 0; f < NS; ++f)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int qi = f * 32 + 8 * g + 4 * hf;
-          const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + kKT + qi);
+          const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + 64 + qi);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float pv = px[(f * 16 + 4 * g + e) * 64 + lane];
@@ -563,10 +611,11 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
     // dV^T += dO^T P (wave A) or dK^T += Q^T dS (wave B)
     const lds_char *Cs = role_a ? Ds : Qs;
 #pragma unroll
-    for (int st = 0; st < kKT / 16; ++st) {
+    for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t pb = pack8(sv[st >> 1], st & 1);
 #pragma unroll
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Cs, nf * 32, st, lane), pb, acc[nf]);
+    }
     }
     block_barrier();  // every wave is done with this buffer and the P slots before they are refilled
   }
@@ -576,26 +625,54 @@ __global__ __launch_bounds__(NG * 128) void attn_bwd_dkdv_kernel(int B, int S, i
                       const_cast<lds_char *>(smem) + wid * 8192, S - k0w);
 }
 
-template <int D>
-void launch_fwd_d(int B, int S, int heads, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
+// Launch shapes.  Forward and dQ: 4 waves of 32 queries per workgroup; dK/dV:
+// NG groups of 32 keys, two waves each.  KT is the token tile streamed
+// through LDS, MINB the workgroups each CU must hold at once (it caps the
+// registers per wave: 512 / (waves per SIMD)).
+constexpr int kFwdKT = 32, kFwdStages = 2, kFwdMinBlocks = 3, kFwdSmallGrid = 256;
+constexpr int kDqWaves = 4, kDqKT = 32, kDqStages = 2, kDqMinBlocks = 2;
+constexpr int kDkvGroups = 2, kDkvKT = 32, kDkvMinBlocks = 3;
+
+template <int D, int KT, int ST, int MINB>
+void launch_fwd_cfg(int B, int S, int heads, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
   const int blocks = B * heads * ((S + kRows - 1) / kRows);
   const uint32_t bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * 3 * heads * D * 2);
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(blocks), dim3(256), 4 * kTileBytes, s, B, S, heads, qkv, bytes, o, lse);
+  // ST stages of (K, V) tiles; the per-wave 8 KB output slots reuse them
+  constexpr int lds = std::max(2 * ST * tile_bytes<KT>(), 4 * 8192);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, KT, ST, MINB>), dim3(blocks), dim3(256), lds, s, B, S, heads, qkv, bytes, o,
+                     lse);
+}
+
+// A grid that leaves CUs idle runs each block's tiles back to back with no
+// other block to hide their latency: there fewer, longer tiles win (64
+// tokens, two blocks per CU); larger grids take 32-token tiles and three
+// blocks per CU.
+template <int D>
+void launch_fwd_d(int B, int S, int heads, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
+  const long blocks = static_cast<long>(B) * heads * ((S + kRows - 1) / kRows);
+  if (blocks <= kFwdSmallGrid)
+    launch_fwd_cfg<D, 64, 2, 2>(B, S, heads, qkv, o, lse, s);
+  else
+    launch_fwd_cfg<D, kFwdKT, kFwdStages, kFwdMinBlocks>(B, S, heads, qkv, o, lse, s);
 }
 
 template <int D>
 void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, const float *lse, const bf16_t *dO,
                   bf16_t *dqkv, float *dvec, hipStream_t s) {
-  constexpr int NWQ = 4, NGK = 4;
   const uint32_t qkv_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * 3 * heads * D * 2);
   const uint32_t do_bytes = static_cast<uint32_t>(static_cast<size_t>(B) * S * heads * D * 2);
-  const int qblocks = B * heads * ((S + 32 * NWQ - 1) / (32 * NWQ));
-  const int kblocks = B * heads * ((S + 32 * NGK - 1) / (32 * NGK));
-  constexpr int kDqLds = 2 * 2 * kTileBytes, kDkvLds = 2 * (2 * kTileBytes + 2 * kKT * 4) + NGK * 8192;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NWQ>), dim3(qblocks), dim3(NWQ * 64), kDqLds, s, B, S, heads,
-                     qkv, qkv_bytes, o, lse, dO, dqkv, dvec);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NGK>), dim3(kblocks), dim3(NGK * 128), kDkvLds, s, B, S, heads, qkv,
-                     qkv_bytes, lse, dO, do_bytes, dvec, dqkv);
+  const int qblocks = B * heads * ((S + 32 * kDqWaves - 1) / (32 * kDqWaves));
+  const int kblocks = B * heads * ((S + 32 * kDkvGroups - 1) / (32 * kDkvGroups));
+  // dQ: kDqStages stages of (K, V) tiles, reused by the per-wave output slots.
+  // dK/dV: two stages of (Q, dO, lse, D) and one 32 x KT fp32 P slot per key
+  // group, or the per-wave output slots if those need more.
+  constexpr int kDqLds = std::max(2 * kDqStages * tile_bytes<kDqKT>(), kDqWaves * 8192);
+  constexpr int kDkvLds = std::max(2 * dkdv_stage_bytes<kDkvKT>() + kDkvGroups * 32 * kDkvKT * 4,
+                                   2 * kDkvGroups * 8192);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kDqWaves, kDqKT, kDqStages, kDqMinBlocks>), dim3(qblocks), dim3(kDqWaves * 64),
+                     kDqLds, s, B, S, heads, qkv, qkv_bytes, o, lse, dO, dqkv, dvec);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, kDkvGroups, kDkvKT, kDkvMinBlocks>), dim3(kblocks),
+                     dim3(kDkvGroups * 128), kDkvLds, s, B, S, heads, qkv, qkv_bytes, lse, dO, do_bytes, dvec, dqkv);
 }
 
 }  // namespace
@@ -603,7 +680,7 @@ void launch_bwd_d(int B, int S, int heads, const bf16_t *qkv, const bf16_t *o, c
 bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *o, float *lse, hipStream_t s) {
   // every tile address (up to one tile past the tensor) must stay a 32-bit buffer offset
   const uint64_t ld = 3ull * heads * d;
-  if ((static_cast<uint64_t>(B) * S + kKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
+  if ((static_cast<uint64_t>(B) * S + kMaxKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
   switch (d) {
     case 64: launch_fwd_d<64>(B, S, heads, qkv, o, lse, s); return true;
     case 80: launch_fwd_d<80>(B, S, heads, qkv, o, lse, s); return true;
@@ -615,7 +692,7 @@ bool launch_attn_fwd(int B, int S, int heads, int d, const bf16_t *qkv, bf16_t *
 bool launch_attn_bwd(int B, int S, int heads, int d, const bf16_t *qkv, const bf16_t *o, const float *lse,
                      const bf16_t *dO, bf16_t *dqkv, float *dvec, hipStream_t s) {
   const uint64_t ld = 3ull * heads * d;
-  if ((static_cast<uint64_t>(B) * S + kKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
+  if ((static_cast<uint64_t>(B) * S + kMaxKT) * ld * 2 + kDL * 2 >= (1ull << 32)) return false;
   switch (d) {
     case 64: launch_bwd_d<64>(B, S, heads, qkv, o, lse, dO, dqkv, dvec, s); return true;
     case 80: launch_bwd_d<80>(B, S, heads, qkv, o, lse, dO, dqkv, dvec, s); return true;
