@@ -741,6 +741,9 @@ class Chain:
         self.g = {n: torch.zeros(tuple(params[n].shape), **f32) for n in params}
         self.ln_ws = e((B.ln_bwd_workspace_bytes(M, H),), dtype=torch.uint8, device=dev)
         self.attn_ws = e((B.attn_bwd_workspace_bytes(Bn, S, nh, d),), dtype=torch.uint8, device=dev)
+        # one workspace for the four weight gradients (split token sums of small outputs)
+        wg = max(B.linear_bwd_weight_workspace_bytes(M, n, k) for n, k in ((H, F), (F, H), (H, A), (3 * A, H)))
+        self.wg_ws = e((max(wg, 256),), dtype=torch.uint8, device=dev)
         self.M, self.A = M, A
         self.kernels = self._kernels()
 
@@ -756,17 +759,21 @@ class Chain:
             ("mlp_up_fwd", lambda: B.enc_mlp_up_fwd(t["y2"], p["w_1"], p["b_1"], t["u"], t["g"])),
             ("mlp_down_fwd", lambda: B.enc_mlp_down_fwd(t["g"], p["w_2"], p["b_2"], t["h"], t["out"])),
             ("mlp_down_bwd_data", lambda: B.enc_mlp_down_bwd_data(dout, p["w_2"], t["u"], t["du"])),
-            ("mlp_down_bwd_weight", lambda: B.enc_mlp_down_bwd_weight(dout, t["g"], g["w_2"], g["b_2"])),
+            ("mlp_down_bwd_weight", lambda: B.enc_mlp_down_bwd_weight(dout, t["g"], g["w_2"], g["b_2"],
+                                                                                  ws=self.wg_ws)),
             ("mlp_up_bwd_data", lambda: B.enc_mlp_up_bwd_data(t["du"], p["w_1"], t["dy2"])),
-            ("mlp_up_bwd_weight", lambda: B.enc_mlp_up_bwd_weight(t["du"], t["y2"], g["w_1"], g["b_1"])),
+            ("mlp_up_bwd_weight", lambda: B.enc_mlp_up_bwd_weight(t["du"], t["y2"], g["w_1"], g["b_1"],
+                                                                              ws=self.wg_ws)),
             ("ln2_bwd", lambda: B.enc_ln_bwd(t["dy2"], t["h"], t["mean2"], t["rstd2"], p["ln2_g"], dout, t["dh"],
                                              g["ln2_g"], g["ln2_b"], ws=self.ln_ws)),
             ("oproj_bwd_data", lambda: B.enc_oproj_bwd_data(t["dh"], p["w_o"], t["do"])),
-            ("oproj_bwd_weight", lambda: B.enc_oproj_bwd_weight(t["dh"], t["o"], g["w_o"], g["b_o"])),
+            ("oproj_bwd_weight", lambda: B.enc_oproj_bwd_weight(t["dh"], t["o"], g["w_o"], g["b_o"],
+                                                                            ws=self.wg_ws)),
             ("attn_bwd", lambda: B.enc_attn_bwd(Bn, S, nh, d, t["qkv"], t["o"], t["lse"], t["do"], t["dqkv"],
                                                 ws=self.attn_ws)),
             ("qkv_bwd_data", lambda: B.enc_qkv_bwd_data(t["dqkv"], p["w_qkv"], t["dy1"])),
-            ("qkv_bwd_weight", lambda: B.enc_qkv_bwd_weight(t["dqkv"], t["y1"], g["w_qkv"], g["b_qkv"])),
+            ("qkv_bwd_weight", lambda: B.enc_qkv_bwd_weight(t["dqkv"], t["y1"], g["w_qkv"], g["b_qkv"],
+                                                                          ws=self.wg_ws)),
             ("ln1_bwd", lambda: B.enc_ln_bwd(t["dy1"], x, t["mean1"], t["rstd1"], p["ln1_g"], t["dh"], t["dx"],
                                              g["ln1_g"], g["ln1_b"], ws=self.ln_ws)),
         ]

@@ -112,7 +112,8 @@ typedef struct {
 const char *enc_status_string(int status);
 /* Description of the last failure on the calling thread ("" if none). */
 const char *enc_last_error(void);
-/* ABI version of this header (bumped on incompatible change). */
+/* ABI version of this header (bumped on incompatible change; 2: workspace
+ * arguments of the weight-gradient entry points). */
 int enc_abi_version(void);
 
 /* ------------------------------------------------------------ sizing */
@@ -244,27 +245,41 @@ int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv,
  * Parameter gradients of a linear layer Y = X W^T + b, summed over the M
  * token rows: dW[N, K] = dY[M, N]^T * X[M, K]; db[N] = sum_m dY[m, :]
  * (db may be NULL).  fp32 outputs are overwritten (accumulate=0) or added
- * to (accumulate=1).  The sums are deterministic (no atomics). */
+ * to (accumulate=1).  The sums are deterministic (no atomics).
+ * ws: NULL, or at least enc_linear_bwd_weight_workspace_bytes(M, N, K)
+ * bytes (else ENC_ERR_WORKSPACE).  When the output's tiles would leave most
+ * of the GPU idle (a small dW with many tokens), a workspace lets the token
+ * sum be split over several workgroups per tile; their fp32 partials are
+ * added in a fixed order, so results stay deterministic for a given shape
+ * and workspace choice.  The size query returns 0 for shapes that never
+ * split.  With ws = NULL nothing is split. */
+int enc_linear_bwd_weight_workspace_bytes(int M, int N, int K, size_t *bytes);
 int enc_linear_bwd_weight(int M, int N, int K, const enc_bf16 *dY,
                           const enc_bf16 *X, float *dW, float *db,
-                          int accumulate, enc_stream_t stream);
-/* The four uses of enc_linear_bwd_weight in the layer, by name:
- *  MLP down: dw_2[H, F] = dout^T g,   db_2[H]
- *  MLP up:   dw_1[F, H] = du^T y2,    db_1[F]
- *  out proj: dw_o[H, A] = dh^T o,     db_o[H]
- *  QKV:      dw_qkv[3A, H] = dqkv^T y1, db_qkv[3A] */
+                          int accumulate, void *ws, size_t ws_bytes,
+                          enc_stream_t stream);
+/* The four uses of enc_linear_bwd_weight in the layer, by name (ws as above,
+ * sized for the same M, N, K):
+ *  MLP down: dw_2[H, F] = dout^T g,   db_2[H]      (N = H, K = F)
+ *  MLP up:   dw_1[F, H] = du^T y2,    db_1[F]      (N = F, K = H)
+ *  out proj: dw_o[H, A] = dh^T o,     db_o[H]      (N = H, K = A)
+ *  QKV:      dw_qkv[3A, H] = dqkv^T y1, db_qkv[3A]  (N = 3A, K = H) */
 int enc_mlp_down_bwd_weight(int M, int F, int H, const enc_bf16 *dout,
                             const enc_bf16 *g, float *dw_2, float *db_2,
-                            int accumulate, enc_stream_t stream);
+                            int accumulate, void *ws, size_t ws_bytes,
+                            enc_stream_t stream);
 int enc_mlp_up_bwd_weight(int M, int H, int F, const enc_bf16 *du,
                           const enc_bf16 *y2, float *dw_1, float *db_1,
-                          int accumulate, enc_stream_t stream);
+                          int accumulate, void *ws, size_t ws_bytes,
+                          enc_stream_t stream);
 int enc_oproj_bwd_weight(int M, int A, int H, const enc_bf16 *dh,
                          const enc_bf16 *o, float *dw_o, float *db_o,
-                         int accumulate, enc_stream_t stream);
+                         int accumulate, void *ws, size_t ws_bytes,
+                         enc_stream_t stream);
 int enc_qkv_bwd_weight(int M, int H, int A, const enc_bf16 *dqkv,
                        const enc_bf16 *y1, float *dw_qkv, float *db_qkv,
-                       int accumulate, enc_stream_t stream);
+                       int accumulate, void *ws, size_t ws_bytes,
+                       enc_stream_t stream);
 
 /* [Backward of LN2 and LN1 with the residual branch (§3.1 decision 3; §4.2)]
  * LayerNorm backward (exact gradient of enc_ln_fwd) with the residual

@@ -86,11 +86,12 @@ _SIGS = {
     "enc_mlp_up_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
     "enc_oproj_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
     "enc_qkv_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
-    "enc_linear_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
-    "enc_mlp_down_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
-    "enc_mlp_up_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
-    "enc_oproj_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
-    "enc_qkv_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p],
+    "enc_linear_bwd_weight_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
+    "enc_linear_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_mlp_down_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_mlp_up_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_oproj_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
+    "enc_qkv_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_ln_bwd": [_i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_attn_bwd": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
     "enc_attn_bwd_noalloc": [_i, _i, _i, _i, _p, _p, _p, _p, _p, _p],
@@ -394,7 +395,26 @@ def enc_qkv_bwd_data(dqkv, w_qkv, dy1=None, stream=None):
     return dy1
 
 
-def enc_linear_bwd_weight(dY, X, dW=None, db=None, accumulate=False, with_db=True, stream=None):
+def linear_bwd_weight_workspace_bytes(M, N, K):
+    n = _sz()
+    _call("enc_linear_bwd_weight_workspace_bytes", M, N, K, ctypes.byref(n))
+    return n.value
+
+
+def _wgrad_ws(M, N, K, ws, split, device):
+    """Workspace argument of a weight-gradient call: a caller tensor, a fresh
+    one of the queried size (split=True, ws=None), or none (split=False)."""
+    if not split:
+        return ctypes.c_void_p(0), 0
+    if ws is None:
+        need = linear_bwd_weight_workspace_bytes(M, N, K)
+        if need == 0:
+            return ctypes.c_void_p(0), 0
+        ws = torch.empty(need, dtype=torch.uint8, device=device)
+    return _ptr(ws), ws.numel() * ws.element_size()
+
+
+def enc_linear_bwd_weight(dY, X, dW=None, db=None, accumulate=False, with_db=True, ws=None, split=True, stream=None):
     M, N = dY.shape
     K = X.shape[1]
     _check(dY, "dY", (M, N))
@@ -404,46 +424,49 @@ def enc_linear_bwd_weight(dY, X, dW=None, db=None, accumulate=False, with_db=Tru
     dW = _out(dW, "dW", (N, K), dY, torch.float32)
     if with_db:
         db = _out(db, "db", (N,), dY, torch.float32)
-    _call("enc_linear_bwd_weight", M, N, K, _ptr(dY), _ptr(X), _ptr(dW), _ptr(db), 1 if accumulate else 0,
+    wp, wn = _wgrad_ws(M, N, K, ws, split, dY.device)
+    _call("enc_linear_bwd_weight", M, N, K, _ptr(dY), _ptr(X), _ptr(dW), _ptr(db), 1 if accumulate else 0, wp, wn,
           _stream(stream))
     return dW, db
 
 
-def _named_wgrad(name, M, a, b, dY, X, dW, db, accumulate, stream):
-    _call(name, M, a, b, _ptr(dY), _ptr(X), _ptr(dW), _ptr(db), 1 if accumulate else 0, _stream(stream))
+def _named_wgrad(name, M, a, b, N, K, dY, X, dW, db, accumulate, ws, split, stream):
+    wp, wn = _wgrad_ws(M, N, K, ws, split, dY.device)
+    _call(name, M, a, b, _ptr(dY), _ptr(X), _ptr(dW), _ptr(db), 1 if accumulate else 0, wp, wn, _stream(stream))
     return dW, db
 
 
-def enc_mlp_down_bwd_weight(dout, g, dw_2, db_2, accumulate=False, stream=None):
+def enc_mlp_down_bwd_weight(dout, g, dw_2, db_2, accumulate=False, ws=None, split=True, stream=None):
     M, H = dout.shape
     F = g.shape[1]
     _check(dout, "dout", (M, H)); _check(g, "g", (M, F))
     _check(dw_2, "dw_2", (H, F), torch.float32); _check(db_2, "db_2", (H,), torch.float32)
-    return _named_wgrad("enc_mlp_down_bwd_weight", M, F, H, dout, g, dw_2, db_2, accumulate, stream)
+    return _named_wgrad("enc_mlp_down_bwd_weight", M, F, H, H, F, dout, g, dw_2, db_2, accumulate, ws, split, stream)
 
 
-def enc_mlp_up_bwd_weight(du, y2, dw_1, db_1, accumulate=False, stream=None):
+def enc_mlp_up_bwd_weight(du, y2, dw_1, db_1, accumulate=False, ws=None, split=True, stream=None):
     M, F = du.shape
     H = y2.shape[1]
     _check(du, "du", (M, F)); _check(y2, "y2", (M, H))
     _check(dw_1, "dw_1", (F, H), torch.float32); _check(db_1, "db_1", (F,), torch.float32)
-    return _named_wgrad("enc_mlp_up_bwd_weight", M, H, F, du, y2, dw_1, db_1, accumulate, stream)
+    return _named_wgrad("enc_mlp_up_bwd_weight", M, H, F, F, H, du, y2, dw_1, db_1, accumulate, ws, split, stream)
 
 
-def enc_oproj_bwd_weight(dh, o, dw_o, db_o, accumulate=False, stream=None):
+def enc_oproj_bwd_weight(dh, o, dw_o, db_o, accumulate=False, ws=None, split=True, stream=None):
     M, H = dh.shape
     A = o.shape[1]
     _check(dh, "dh", (M, H)); _check(o, "o", (M, A))
     _check(dw_o, "dw_o", (H, A), torch.float32); _check(db_o, "db_o", (H,), torch.float32)
-    return _named_wgrad("enc_oproj_bwd_weight", M, A, H, dh, o, dw_o, db_o, accumulate, stream)
+    return _named_wgrad("enc_oproj_bwd_weight", M, A, H, H, A, dh, o, dw_o, db_o, accumulate, ws, split, stream)
 
 
-def enc_qkv_bwd_weight(dqkv, y1, dw_qkv, db_qkv, accumulate=False, stream=None):
+def enc_qkv_bwd_weight(dqkv, y1, dw_qkv, db_qkv, accumulate=False, ws=None, split=True, stream=None):
     M, A3 = dqkv.shape
     H = y1.shape[1]
     _check(dqkv, "dqkv", (M, A3)); _check(y1, "y1", (M, H))
     _check(dw_qkv, "dw_qkv", (A3, H), torch.float32); _check(db_qkv, "db_qkv", (A3,), torch.float32)
-    return _named_wgrad("enc_qkv_bwd_weight", M, H, A3 // 3, dqkv, y1, dw_qkv, db_qkv, accumulate, stream)
+    return _named_wgrad("enc_qkv_bwd_weight", M, H, A3 // 3, A3, H, dqkv, y1, dw_qkv, db_qkv, accumulate, ws, split,
+                        stream)
 
 
 def enc_ln_bwd(dy, x, mean, rstd, gamma, dresid=None, dx=None, dgamma=None, dbeta=None, accumulate=False,

@@ -3,6 +3,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "../../include/optimus_enc.h"
@@ -151,8 +152,15 @@ void saved_layout(const enc_cfg_t *c, enc_saved_layout_t *L) {
 
 // Backward workspace regions (offsets in bytes).
 struct BwdWs {
-  size_t du, dy2, dh, dO, dqkv, dy1, ln_part, dvec, total;
+  size_t du, dy2, dh, dO, dqkv, dy1, ln_part, dvec, wg, wg_bytes, total;
 };
+
+// Workspace of the four weight gradients of a layer (each uses it in turn).
+size_t layer_wgrad_ws(const enc_cfg_t *c) {
+  const int M = c->batch * c->seq, H = c->hidden, A = c->heads * c->head_dim, F = c->mlp;
+  return std::max(std::max(gemm_wgrad_ws_bytes(H, F, M), gemm_wgrad_ws_bytes(F, H, M)),
+                  std::max(gemm_wgrad_ws_bytes(H, A, M), gemm_wgrad_ws_bytes(3 * A, H, M)));
+}
 
 BwdWs bwd_layout(const enc_cfg_t *c) {
   const size_t M = static_cast<size_t>(c->batch) * c->seq;
@@ -172,6 +180,8 @@ BwdWs bwd_layout(const enc_cfg_t *c) {
   w.dy1 = take(M * H * 2);
   w.ln_part = take(ln_bwd_ws_bytes(static_cast<int>(M), c->hidden));
   w.dvec = take(attn_bwd_ws_bytes(c->batch, c->seq, c->heads));
+  w.wg_bytes = layer_wgrad_ws(c);
+  w.wg = take(w.wg_bytes);
   w.total = off;
   return w;
 }
@@ -234,12 +244,13 @@ bool gemm_dgrad_add(int M, int N, int K, const bf16_t *dY, const bf16_t *W, cons
 }
 
 // dW[N, K] (+)= dY[M, N]^T X[M, K]; db[N] (+)= sum_m dY
-bool gemm_wgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *X, float *dW, float *db, int acc, hipStream_t s) {
+bool gemm_wgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *X, float *dW, float *db, int acc, void *ws,
+                size_t ws_bytes, hipStream_t s) {
   GemmArgs a{};
   a.M = N, a.N = K, a.K = M;
   a.A = dY, a.lda = N, a.B = X, a.ldb = K;
   a.Wf = dW, a.ldy = K, a.db = db, a.accumulate = acc;
-  return launch_gemm_wgrad(a, s);
+  return launch_gemm_wgrad(a, ws, ws_bytes, s);
 }
 
 int linear_dims(const char *fn, int M, std::initializer_list<int> feats) {
@@ -409,7 +420,7 @@ const char *enc_status_string(int status) {
 
 const char *enc_last_error(void) { return g_last_error.c_str(); }
 
-int enc_abi_version(void) { return 1; }
+int enc_abi_version(void) { return 2; }
 
 int enc_saved_layout(const enc_cfg_t *cfg, enc_saved_layout_t *layout) {
   int r = check_cfg("enc_saved_layout", cfg);
@@ -591,38 +602,50 @@ int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf
   return launched(fn);
 }
 
+int enc_linear_bwd_weight_workspace_bytes(int M, int N, int K, size_t *bytes) {
+  const char *fn = "enc_linear_bwd_weight_workspace_bytes";
+  int r = linear_dims(fn, M, {N, K});
+  if (r) return r;
+  if (static_cast<long>(N) * K >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: dW exceeds 2^31 elements", fn);
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = gemm_wgrad_ws_bytes(N, K, M);
+  return ok();
+}
+
 int enc_linear_bwd_weight(int M, int N, int K, const enc_bf16 *dY, const enc_bf16 *X, float *dW, float *db,
-                          int accumulate, enc_stream_t stream) {
+                          int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_linear_bwd_weight";
   int r = linear_dims(fn, M, {N, K});
   if (r) return r;
   if (static_cast<long>(N) * K >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: dW exceeds 2^31 elements", fn);
   PtrCheck c(fn);
-  c.req(dY, "dY").req(X, "X").req(dW, "dW").opt(db, "db");
+  c.req(dY, "dY").req(X, "X").req(dW, "dW").opt(db, "db").opt(ws, "ws");
   if (c.code) return c.code;
-  if (!gemm_wgrad(M, N, K, dY, X, dW, db, accumulate ? 1 : 0, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  const size_t need = gemm_wgrad_ws_bytes(N, K, M);
+  if (ws && ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
+  if (!gemm_wgrad(M, N, K, dY, X, dW, db, accumulate ? 1 : 0, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
 int enc_mlp_down_bwd_weight(int M, int F, int H, const enc_bf16 *dout, const enc_bf16 *g, float *dw_2, float *db_2,
-                            int accumulate, enc_stream_t stream) {
-  return enc_linear_bwd_weight(M, H, F, dout, g, dw_2, db_2, accumulate, stream);
+                            int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, H, F, dout, g, dw_2, db_2, accumulate, ws, ws_bytes, stream);
 }
 
 int enc_mlp_up_bwd_weight(int M, int H, int F, const enc_bf16 *du, const enc_bf16 *y2, float *dw_1, float *db_1,
-                          int accumulate, enc_stream_t stream) {
-  return enc_linear_bwd_weight(M, F, H, du, y2, dw_1, db_1, accumulate, stream);
+                          int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, F, H, du, y2, dw_1, db_1, accumulate, ws, ws_bytes, stream);
 }
 
 int enc_oproj_bwd_weight(int M, int A, int H, const enc_bf16 *dh, const enc_bf16 *o, float *dw_o, float *db_o,
-                         int accumulate, enc_stream_t stream) {
-  return enc_linear_bwd_weight(M, H, A, dh, o, dw_o, db_o, accumulate, stream);
+                         int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, H, A, dh, o, dw_o, db_o, accumulate, ws, ws_bytes, stream);
 }
 
 int enc_qkv_bwd_weight(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *y1, float *dw_qkv, float *db_qkv,
-                       int accumulate, enc_stream_t stream) {
-  return enc_linear_bwd_weight(M, 3 * A, H, dqkv, y1, dw_qkv, db_qkv, accumulate, stream);
+                       int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
+  return enc_linear_bwd_weight(M, 3 * A, H, dqkv, y1, dw_qkv, db_qkv, accumulate, ws, ws_bytes, stream);
 }
 
 int enc_ln_bwd(int rows, int cols, const enc_bf16 *dy, const enc_bf16 *x, const float *mean, const float *rstd,
@@ -745,17 +768,18 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   bf16_t *du = at<bf16_t>(ws, W.du), *dy2 = at<bf16_t>(ws, W.dy2), *dh = at<bf16_t>(ws, W.dh);
   bf16_t *dO = at<bf16_t>(ws, W.dO), *dqkv = at<bf16_t>(ws, W.dqkv), *dy1 = at<bf16_t>(ws, W.dy1);
   float *part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec);
+  void *wg = W.wg_bytes ? at<char>(ws, W.wg) : nullptr;  // split weight-gradient partials
 
   bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                      // du = dout W2 * GELU'(u)
-  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, s);          // dW2, db2
+  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, wg, W.wg_bytes, s);          // dW2, db2
   okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy2, s);               // dy2 = du W1
-  okk = okk && gemm_wgrad(M, F, H, du, y2, gr.w_1, gr.b_1, acc, s);           // dW1, db1
+  okk = okk && gemm_wgrad(M, F, H, du, y2, gr.w_1, gr.b_1, acc, wg, W.wg_bytes, s);           // dW1, db1
   okk = okk && launch_ln_bwd(M, H, dy2, h, mean2, rstd2, p.ln2_g, dout, dh, gr.ln2_g, gr.ln2_b, acc, part, s);
   okk = okk && gemm_dgrad(M, H, A, dh, p.w_o, nullptr, dO, s);                // dO = dh Wo
-  okk = okk && gemm_wgrad(M, H, A, dh, o, gr.w_o, gr.b_o, acc, s);            // dWo, dbo
+  okk = okk && gemm_wgrad(M, H, A, dh, o, gr.w_o, gr.b_o, acc, wg, W.wg_bytes, s);            // dWo, dbo
   okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkv, o, lse, dO, dqkv, dvec, s);
   okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, s);       // dy1 = dqkv Wqkv
-  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, s);  // dWqkv, dbqkv
+  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, wg, W.wg_bytes, s);  // dWqkv, dbqkv
   okk = okk && launch_ln_bwd(M, H, dy1, x, mean1, rstd1, p.ln1_g, dh, dx, gr.ln1_g, gr.ln1_b, acc, part, s);
   if (!okk) return refused_after_checks(fn);
   return launched(fn);
@@ -883,15 +907,15 @@ int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   float *ln_part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec), *qk_part = at<float>(ws, W.qk_part);
 
   bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                  // du = dout W2 * GELU'(u)
-  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, s);      // dW2, db2
+  okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, nullptr, 0, s);      // dW2, db2
   okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy_mlp, s);        // MLP branch's dy
-  okk = okk && gemm_wgrad(M, F, H, du, y, gr.w_1, gr.b_1, acc, s);        // dW1, db1
+  okk = okk && gemm_wgrad(M, F, H, du, y, gr.w_1, gr.b_1, acc, nullptr, 0, s);        // dW1, db1
   okk = okk && gemm_dgrad(M, H, A, dout, p.w_o, nullptr, dO, s);          // dO = dout Wo
-  okk = okk && gemm_wgrad(M, H, A, dout, o, gr.w_o, gr.b_o, acc, s);      // dWo, dbo
+  okk = okk && gemm_wgrad(M, H, A, dout, o, gr.w_o, gr.b_o, acc, nullptr, 0, s);      // dWo, dbo
   okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkvn, o, lse, dO, dqkvn, dvec, s);
   okk = okk && launch_qk_norm_bwd(M, cfg->heads, cfg->head_dim, dqkvn, qkv, qks, p.qn_g, p.kn_g, dqkv, gr.qn_g,
                                   gr.qn_b, gr.kn_g, gr.kn_b, acc, qk_part, s);
-  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y, gr.w_qkv, nullptr, acc, s);  // dWqkv (no bias)
+  okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y, gr.w_qkv, nullptr, acc, nullptr, 0, s);  // dWqkv (no bias)
   okk = okk && gemm_dgrad_add(M, 3 * A, H, dqkv, p.w_qkv, dy_mlp, dy, s);   // dy = dqkv Wqkv + dy_mlp
   okk = okk && launch_ln_bwd(M, H, dy, x, mean, rstd, p.ln_g, dout, dx, gr.ln_g, gr.ln_b, acc, ln_part, s);
   if (!okk) return refused_after_checks(fn);
@@ -955,7 +979,7 @@ int enc_patch_embed_bwd(int batch, int channels, int img_h, int img_w, int patch
     okk = okk && launch_patch_token_rows(batch, N, S, hidden, dx0, static_cast<bf16_t *>(ws), s);
     dtok = static_cast<const bf16_t *>(ws);
   }
-  okk = okk && gemm_wgrad(batch * N, hidden, Kp, dtok, patches, dw_pe, db_pe, acc, s);
+  okk = okk && gemm_wgrad(batch * N, hidden, Kp, dtok, patches, dw_pe, db_pe, acc, nullptr, 0, s);
   if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }

@@ -25,6 +25,8 @@
 // Workgroup order is XCD-aware: MI355X dispatches workgroup i to XCD i % 8,
 // so each XCD is given its own block of the tile grid, walked M-fastest in
 // groups of row tiles, which keeps the operand panels it shares in its L2.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "lds_dma.hpp"
@@ -73,8 +75,7 @@ __device__ __forceinline__ float gelu_grad_f(float u) {
 // 8 row tiles.  (Measured on the twelve ViT-22B layer GEMMs: 0.7% less time
 // in total than the contiguous order, from 5% on the MLP-up weight gradient
 // to -2% on the QKV weight gradient.)
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int &tm, int &tn) {
-  const int pid = blockIdx.x, nb = gridDim.x;
+__device__ __forceinline__ void tile_of(int pid, int nb, int tiles_m, int tiles_n, int &tm, int &tn) {
   const int xcd = pid & 7, local = pid >> 3;
   if (tiles_m % 2 == 0 && tiles_n % 4 == 0) {
     constexpr int GM = 4;
@@ -97,6 +98,49 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int &tm, int &
   const int in_g = logical - g * group_size;
   tm = first_m + in_g % gm;
   tn = in_g / gm;
+}
+
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int &tm, int &tn) {
+  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+}
+
+// Split of the contraction handled by this workgroup.  With p.splits > 1 the
+// grid holds splits x tiles work items, listed split-major and M-fastest
+// within a split; each XCD (workgroup i runs on XCD i % 8) takes one
+// contiguous range of that list, so the items on one XCD mostly share a
+// split and with it the operand panels of its k-range (the tiles of one
+// tile column share the weight-gradient rows' panel, those of one tile row
+// the other operand's).  Returns the split; kbeg/klen give its contraction
+// range.
+__device__ __forceinline__ int split_of(const GemmArgs &p, int tiles_m, int tiles_n, int &tm, int &tn, int &kbeg,
+                                       int &klen) {
+  if (p.splits > 1) {
+    const int nt = tiles_m * tiles_n;
+    const int pid = blockIdx.x, nb = gridDim.x;
+    const int xcd = pid & 7, local = pid >> 3, per = nb >> 3, rem = nb & 7;
+    const int item = (xcd < rem) ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+    const int split = item / nt, t = item - split * nt;
+    tm = t % tiles_m;
+    tn = t / tiles_m;
+    kbeg = split * p.k_chunk;
+    klen = min(p.K - kbeg, p.k_chunk);
+    return split;
+  }
+  tile_of(tiles_m, tiles_n, tm, tn);
+  kbeg = 0;
+  klen = p.K;
+  return 0;
+}
+
+// Output pointers of split `split`: its own partial slice, overwritten.
+__device__ __forceinline__ GemmArgs split_outputs(const GemmArgs &p, int split) {
+  GemmArgs q = p;
+  if (p.splits > 1) {
+    q.Wf = p.Wf + static_cast<size_t>(split) * p.split_stride;
+    if (q.db) q.db = p.db + static_cast<size_t>(split) * p.M;
+    q.accumulate = 0;
+  }
+  return q;
 }
 
 // Epilogue of one wave tile: lane owns row m and columns nb..nb+3 of each
@@ -647,17 +691,19 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int wm = wid / WN, wn = wid % WN;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
-  int tm, tn;
-  tile_of(tiles_m, tiles_n, tm, tn);
+  int tm, tn, kbeg, klen;
+  const int split = split_of(p, tiles_m, tiles_n, tm, tn, kbeg, klen);
   const int m0 = tm * BM, n0 = tn * BN;
 
   DirectLoader<BM, BK, NW, AT> la;
   DirectLoader<BN, BK, NW, BT> lb;
   la.init(p.A, a_bytes, p.lda, m0, wid, lane);
   lb.init(p.B, b_bytes, p.ldb, n0, wid, lane);
-  // byte step of one k-step along each operand
+  // byte step of one k-step along each operand, and of the split's first k
   const uint32_t a_step = AT ? static_cast<uint32_t>(BK) * p.lda * 2 : BK * 2;
   const uint32_t b_step = BT ? static_cast<uint32_t>(BK) * p.ldb * 2 : BK * 2;
+  const uint32_t a_k0 = AT ? static_cast<uint32_t>(kbeg) * p.lda * 2 : static_cast<uint32_t>(kbeg) * 2;
+  const uint32_t b_k0 = BT ? static_cast<uint32_t>(kbeg) * p.ldb * 2 : static_cast<uint32_t>(kbeg) * 2;
 
   FragAddr<BM, BK, FM, AT> fa;
   FragAddr<BN, BK, FN, BT> fb;
@@ -679,14 +725,14 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
 #pragma unroll
   for (int i = 0; i < FM; ++i) dbacc[i] = 0.f;
 
-  const int nk = (p.K + BK - 1) / BK;
+  const int nk = (klen + BK - 1) / BK;
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s) {
     if (s < nk) {
-      la.issue(lds0 + s * STAGE, s * a_step, wid);
-      lb.issue(lds0 + s * STAGE + A_BYTES, s * b_step, wid);
+      la.issue(lds0 + s * STAGE, a_k0 + s * a_step, wid);
+      lb.issue(lds0 + s * STAGE + A_BYTES, b_k0 + s * b_step, wid);
     }
   }
   // k-step 0 resident for every wave
@@ -725,8 +771,8 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
     constexpr bool kALate = kSpread && !BT;
     const bool spread = kSpread && (BT || p.K <= 8192);
     if (tl < nk) {
-      if (!kALate || !spread) la.issue(st_l, tl * a_step, wid);
-      if (!kSpread || kALate || !spread) lb.issue(st_l + A_BYTES, tl * b_step, wid);
+      if (!kALate || !spread) la.issue(st_l, a_k0 + tl * a_step, wid);
+      if (!kSpread || kALate || !spread) lb.issue(st_l + A_BYTES, b_k0 + tl * b_step, wid);
     }
     const lds_char *As = smem + (t % STAGES) * STAGE;
 #pragma unroll
@@ -735,9 +781,9 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       if constexpr (kSpread) {
         if (kk == 1 && tl < nk && spread) {
           if constexpr (kALate)
-            la.issue(st_l, tl * a_step, wid);
+            la.issue(st_l, a_k0 + tl * a_step, wid);
           else
-            lb.issue(st_l + A_BYTES, tl * b_step, wid);
+            lb.issue(st_l + A_BYTES, b_k0 + tl * b_step, wid);
         }
       }
 #pragma unroll
@@ -784,7 +830,8 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       for (int j = 0; j < FN; ++j) bfr[0][j] = bfr[1][j];
     }
   }
-  store_tile_lds<EPI, BM, BN, WM, WN>(p, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
+  const GemmArgs q = split_outputs(p, split);
+  store_tile_lds<EPI, BM, BN, WM, WN>(q, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
   if constexpr (kDb) {
     if (do_db) {
       // lane l and l ^ 32 hold the two token halves of row (l % 32)
@@ -792,7 +839,7 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
       for (int i = 0; i < FM; ++i) {
         const float tot = dbacc[i] + __shfl_xor(dbacc[i], 32, kWave);
         const int row = m0 + wm * WTM + i * 32 + (lane & 31);
-        if (lane < 32 && row < p.M) p.db[row] = p.accumulate ? p.db[row] + tot : tot;
+        if (lane < 32 && row < q.M) q.db[row] = q.accumulate ? q.db[row] + tot : tot;
       }
     }
   }
@@ -804,7 +851,7 @@ bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipSt
   constexpr size_t lds = static_cast<size_t>(STAGES) *
                          (DirectLoader<BM, BK, NW, AT>::BYTES + DirectLoader<BN, BK, NW, BT>::BYTES);
   static_assert(lds <= 160 * 1024, "LDS budget");
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (a.splits > 1 ? a.splits : 1);
   hipLaunchKernelGGL((gemm_lds_kernel<BM, BN, BK, WM, WN, STAGES, AT, BT, EPI>), dim3(tiles), dim3(WM * WN * 64),
                      lds, s, a, a_bytes, b_bytes);
   return true;
@@ -861,8 +908,8 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uin
   const int grp = wid >> 2;                                          // 0: waves 0-3, 1: waves 4-7
   const int wm = wid / WN, wn = wid % WN;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
-  int tm, tn;
-  tile_of(tiles_m, tiles_n, tm, tn);
+  int tm, tn, kbeg, klen;
+  const int split = split_of(p, tiles_m, tiles_n, tm, tn, kbeg, klen);
   const int m0 = tm * BM, n0 = tn * BN;
 
   DirectLoader<BM, BK, NW, AT> la;
@@ -871,6 +918,8 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uin
   lb.init(p.B, b_bytes, p.ldb, n0, wid, lane);
   const uint32_t a_step = AT ? static_cast<uint32_t>(BK) * p.lda * 2 : BK * 2;
   const uint32_t b_step = BT ? static_cast<uint32_t>(BK) * p.ldb * 2 : BK * 2;
+  const uint32_t a_k0 = AT ? static_cast<uint32_t>(kbeg) * p.lda * 2 : static_cast<uint32_t>(kbeg) * 2;
+  const uint32_t b_k0 = BT ? static_cast<uint32_t>(kbeg) * p.ldb * 2 : static_cast<uint32_t>(kbeg) * 2;
   FragAddr<BM, BK, FM, AT> fa;
   FragAddr<BN, BK, FN, BT> fb;
   fa.init(wm * WTM, lane);
@@ -887,14 +936,14 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uin
 #pragma unroll
   for (int i = 0; i < FM; ++i) dbacc[i] = 0.f;
 
-  const int nk = (p.K + BK - 1) / BK;
+  const int nk = (klen + BK - 1) / BK;
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   constexpr int PER_STAGE = DirectLoader<BM, BK, NW, AT>::NI + DirectLoader<BN, BK, NW, BT>::NI;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s) {
     if (s < nk) {
-      la.issue(lds0 + s * STAGE, s * a_step, wid);
-      lb.issue(lds0 + s * STAGE + A_BYTES, s * b_step, wid);
+      la.issue(lds0 + s * STAGE, a_k0 + s * a_step, wid);
+      lb.issue(lds0 + s * STAGE + A_BYTES, b_k0 + s * b_step, wid);
     }
   }
   // k-step 0 resident for every wave
@@ -918,8 +967,8 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uin
     const int tl = t + STAGES - 1;
     if (tl < nk) {
       const uint32_t st = lds0 + (tl % STAGES) * STAGE;
-      la.issue(st, tl * a_step, wid);
-      lb.issue(st + A_BYTES, tl * b_step, wid);
+      la.issue(st, a_k0 + tl * a_step, wid);
+      lb.issue(st + A_BYTES, b_k0 + tl * b_step, wid);
     }
     const lds_char *As = smem + (t % STAGES) * STAGE;
 #pragma unroll
@@ -957,14 +1006,15 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_pp_kernel(GemmArgs p, uin
   }
   if (grp == 0) barrier();  // match group 1's extra barrier
 
-  store_tile_lds<EPI, BM, BN, WM, WN>(p, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
+  const GemmArgs q = split_outputs(p, split);
+  store_tile_lds<EPI, BM, BN, WM, WN>(q, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
   if constexpr (kDb) {
     if (do_db) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const float tot = dbacc[i] + __shfl_xor(dbacc[i], 32, kWave);
         const int row = m0 + wm * WTM + i * 32 + (lane & 31);
-        if (lane < 32 && row < p.M) p.db[row] = p.accumulate ? p.db[row] + tot : tot;
+        if (lane < 32 && row < q.M) q.db[row] = q.accumulate ? q.db[row] + tot : tot;
       }
     }
   }
@@ -976,7 +1026,7 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
   constexpr size_t lds = static_cast<size_t>(STAGES) *
                          (DirectLoader<BM, BK, NW, AT>::BYTES + DirectLoader<BN, BK, NW, BT>::BYTES);
   static_assert(lds <= 160 * 1024, "LDS budget");
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (a.splits > 1 ? a.splits : 1);
   hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, BK, WM, WN, STAGES, AT, BT, EPI>), dim3(tiles), dim3(NW * 64), lds, s, a,
                      a_bytes, b_bytes);
   return true;
@@ -996,7 +1046,7 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 // better than the two-stage kernel.
 // Returns false when the operands do not fit the path's constraints.
 template <bool AT, bool BT, Epi EPI>
-bool launch_lds(const GemmArgs &a, hipStream_t s) {
+bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
   constexpr int BK = 64;
   if ((!AT || !BT) && a.K % BK != 0) return false;  // contiguous-k operands need whole k-steps
   // operand tensor extents (bytes) bound the buffer loads; keep every offset < 2^32
@@ -1005,21 +1055,23 @@ bool launch_lds(const GemmArgs &a, hipStream_t s) {
   const uint64_t a_bytes = a_rows * a.lda * 2, b_bytes = b_rows * a.ldb * 2;
   const uint64_t lim = (1ull << 32) - 1;
   if (a_bytes + 600ull * a.lda * 2 > lim || b_bytes + 600ull * a.ldb * 2 > lim) return false;
-  auto cost = [&](int bm, int bn, double eff) {
-    const long tiles = static_cast<long>((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
-    return static_cast<double>((tiles + 255) / 256) * bm * bn / eff;
-  };
-  const double cL = cost(256, 256, 1.0), cM = cost(256, 192, 0.95), cS = cost(128, 128, 0.75);
   const uint32_t ab = static_cast<uint32_t>(a_bytes), bb = static_cast<uint32_t>(b_bytes);
-  if (cL <= cM && cL <= cS) {
+  if (t.bm == 256 && t.bn == 256) {
     if constexpr (BT) return launch_pp_cfg<256, 256, 32, 2, 4, 4, AT, BT, EPI>(a, ab, bb, s);
     return launch_lds_cfg<256, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);
   }
-  if (cM <= cS) {
+  if (t.bm == 256 && t.bn == 192) {
     if constexpr (AT && BT) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
     return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
   }
+  if (t.bm == 256) return launch_lds_cfg<256, 128, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
+  if (t.bn == 256) return launch_lds_cfg<128, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);
   return launch_lds_cfg<128, 128, BK, 2, 2, 2, AT, BT, EPI>(a, ab, bb, s);
+}
+
+template <bool AT, bool BT, Epi EPI>
+bool launch_lds(const GemmArgs &a, hipStream_t s) {
+  return launch_lds<AT, BT, EPI>(a, s, choose_tile(a.M, a.N));
 }
 
 }  // namespace
@@ -1050,8 +1102,48 @@ bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s) {
   }
 }
 
-bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s) {
+namespace {
+
+// out[i] = (accumulate ? out[i] : 0) + part[0][i] + part[1][i] + ... in split
+// order (deterministic), over n4 float4s; blockIdx.y picks the dW or the db
+// segment.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(float *__restrict__ w, const float *__restrict__ wp,
+                                                            long w4, float *__restrict__ b,
+                                                            const float *__restrict__ bp, long b4, int splits,
+                                                            int accumulate) {
+  float *out = blockIdx.y == 0 ? w : b;
+  const float *part = blockIdx.y == 0 ? wp : bp;
+  const long n4 = blockIdx.y == 0 ? w4 : b4;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n4; i += static_cast<long>(gridDim.x) * 256) {
+    f32x4_t v = accumulate ? reinterpret_cast<const f32x4_t *>(out)[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < splits; ++sp) v += reinterpret_cast<const f32x4_t *>(part)[sp * n4 + i];
+    reinterpret_cast<f32x4_t *>(out)[i] = v;
+  }
+}
+
+}  // namespace
+
+bool launch_gemm_wgrad(const GemmArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
   // both paths fuse the bias gradient into the weight-gradient kernel
+  const SplitPlan sp = wgrad_split_plan(a.M, a.N, a.K);
+  if (sp.splits > 1 && ws != nullptr && ws_bytes >= gemm_wgrad_ws_bytes(a.M, a.N, a.K) && a.ldy == a.N &&
+      a.M % 4 == 0 && a.N % 4 == 0) {
+    GemmArgs b = a;
+    b.splits = sp.splits;
+    b.k_chunk = sp.k_chunk;
+    b.split_stride = static_cast<size_t>(a.M) * a.N;
+    b.Wf = static_cast<float *>(ws);
+    b.db = a.db ? b.Wf + ws_round256(static_cast<size_t>(sp.splits) * a.M * a.N * sizeof(float)) / sizeof(float)
+                : nullptr;
+    b.accumulate = 0;
+    if (launch_lds<true, true, Epi::kF32>(b, s, sp.tile)) {
+      const long w4 = static_cast<long>(a.M) * a.N / 4, b4 = a.db ? a.M / 4 : 0;
+      const int blocks = static_cast<int>(std::min<long>((w4 + 255) / 256, 2048));
+      hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks, a.db ? 2 : 1), dim3(256), 0, s, a.Wf, b.Wf, w4, a.db,
+                         b.db, b4, sp.splits, a.accumulate);
+      return true;
+    }
+  }
   return launch_lds<true, true, Epi::kF32>(a, s) || launch_any<true, true, Epi::kF32>(a, s);
 }
 

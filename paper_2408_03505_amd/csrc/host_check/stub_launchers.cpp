@@ -19,7 +19,7 @@ bool launch_ln_bwd(int, int, const bf16_t *, const bf16_t *, const float *, cons
 }
 bool launch_gemm_fwd(const GemmArgs &, Epi, hipStream_t) { return true; }
 bool launch_gemm_dgrad(const GemmArgs &, Epi, hipStream_t) { return true; }
-bool launch_gemm_wgrad(const GemmArgs &, hipStream_t) { return true; }
+bool launch_gemm_wgrad(const GemmArgs &, void *, size_t, hipStream_t) { return true; }
 bool launch_qk_norm_fwd(int, int, int, const bf16_t *, const bf16_t *, const bf16_t *, const bf16_t *,
                         const bf16_t *, float, bf16_t *, float *, hipStream_t) {
   return true;

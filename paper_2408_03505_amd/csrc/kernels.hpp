@@ -45,6 +45,13 @@ struct GemmArgs {
   float *Wf;           // fp32 output [M, ldy]
   float *db;           // fused row sums of A over k (fp32, [M]) for the weight gradient
   int accumulate;
+  // Split contraction (weight gradients only): when splits > 1, workgroup
+  // split s of a tile covers k in [s * k_chunk, min(K, (s + 1) * k_chunk))
+  // (k_chunk a multiple of the k-step) and writes its fp32 partial to
+  // Wf + s * split_stride and db + s * M, overwriting.
+  int splits;
+  int k_chunk;
+  size_t split_stride;
 };
 
 // Forward projections: A = X [M, K] row-major, B = W [N, K] row-major.
@@ -52,7 +59,11 @@ bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s);
 // Input gradient: A = dY [M, K] row-major, B(n, k) = W[k, n] (W stored [K, N]).
 bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s);
 // Weight gradient: A(m, k) = dY[k, m], B(n, k) = X[k, n] (contraction over tokens).
-bool launch_gemm_wgrad(const GemmArgs &a, hipStream_t s);
+// With a workspace of at least gemm_wgrad_ws_bytes(M, N, K) bytes, a problem
+// whose output tiles leave most CUs idle splits the token contraction over
+// several workgroups per tile and adds the fp32 partials in a fixed order;
+// ws = nullptr never splits.
+bool launch_gemm_wgrad(const GemmArgs &a, void *ws, size_t ws_bytes, hipStream_t s);
 
 // ---- QK normalisation (LayerNorm of every query and key vector over head_dim)
 bool launch_qk_norm_fwd(int M, int heads, int d, const bf16_t *qkv, const bf16_t *qg, const bf16_t *qb,

@@ -22,6 +22,7 @@ if not hasattr(L, "enc_host_stub_build"):
 P = ctypes.c_void_p(0x10000)
 S0 = ctypes.c_void_p(0)
 CFGS = [dict(batch=8, seq=256, hidden=6144, heads=48, head_dim=128, mlp=24576, ln_eps=1e-6),
+        dict(batch=32, seq=197, hidden=768, heads=12, head_dim=64, mlp=3072, ln_eps=1e-6),
         dict(batch=2, seq=197, hidden=192, heads=3, head_dim=64, mlp=768, ln_eps=1e-6),
         dict(batch=3, seq=33, hidden=256, heads=2, head_dim=80, mlp=320, ln_eps=1e-5)]
 
@@ -73,11 +74,14 @@ def test_per_kernel_entry_points_run():
     _ok("enc_mlp_up_bwd_data", M, H, F, P, P, P, S0)
     _ok("enc_oproj_bwd_data", M, A, H, P, P, P, S0)
     _ok("enc_qkv_bwd_data", M, H, A, P, P, P, S0)
-    _ok("enc_linear_bwd_weight", M, F, H, P, P, P, P, 1, S0)
-    _ok("enc_linear_bwd_weight", M, F, H, P, P, P, S0, 0, S0)  # no bias gradient
+    _ok("enc_linear_bwd_weight", M, F, H, P, P, P, P, 1, S0, 0, S0)
+    _ok("enc_linear_bwd_weight", M, F, H, P, P, P, S0, 0, S0, 0, S0)  # no bias gradient
+    # a split weight gradient (small output, many tokens) with its workspace
+    need = B.linear_bwd_weight_workspace_bytes(6304, 768, 768)
+    _ok("enc_linear_bwd_weight", 6304, 768, 768, P, P, P, P, 1, P, need, S0)
     for name, n, k in (("enc_mlp_down_bwd_weight", F, H), ("enc_mlp_up_bwd_weight", H, F),
                        ("enc_oproj_bwd_weight", A, H), ("enc_qkv_bwd_weight", H, A)):
-        _ok(name, M, n, k, P, P, P, P, 0, S0)
+        _ok(name, M, n, k, P, P, P, P, 0, S0, 0, S0)
     _ok("enc_ln_bwd", M, H, P, P, P, P, P, S0, P, P, P, 0, P, B.ln_bwd_workspace_bytes(M, H), S0)
     _ok("enc_attn_bwd", 2, 197, 3, 64, P, P, P, P, P, P, B.attn_bwd_workspace_bytes(2, 197, 3, 64), S0)
     _ok("enc_attn_bwd_noalloc", 2, 197, 3, 64, P, P, P, P, P, S0)

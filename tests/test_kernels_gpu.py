@@ -255,8 +255,10 @@ def test_mlp_down_bwd_data_gelu_grad():
 
 
 # wgrad: dW[N, K] = dY[M, N]^T X[M, K], contraction over M tokens
+# (6304, 768, 256), (2048, 1280, 200), (2000, 768, 256) ragged, (6304, 3072, 768)
+# and (4112, 1280, 1280) split the token contraction (outputs of 3-36 tiles).
 WGRAD_SHAPES = [(394, 576, 192), (130, 4096, 4096), (6304, 768, 256), (65, 8, 8), (2048, 1280, 200),
-                (2048, 6144, 1536)]
+                (2048, 6144, 1536), (2000, 768, 256), (6304, 3072, 768), (4112, 1280, 1280)]
 
 
 @pytest.mark.parametrize("M,N,K", WGRAD_SHAPES)
@@ -281,6 +283,32 @@ def test_linear_bwd_weight_exact(M, N, K):
     assert ok, err
     ok, err = exact_equal(db, 2 * rdb)
     assert ok, err
+
+
+@pytest.mark.parametrize("M,N,K", [(6304, 768, 768), (2000, 768, 256), (4112, 1280, 1280)])
+def test_linear_bwd_weight_split_matches_unsplit(M, N, K):
+    # The split plan applies to these shapes; the unsplit kernel is the same
+    # product summed in one pass.  Both within fp32 rounding of float64, and
+    # the split path is run-to-run bitwise deterministic.
+    assert B.linear_bwd_weight_workspace_bytes(M, N, K) > 0
+    announce(f"bwd_weight split vs unsplit M={M} N={N} K={K}")
+    dY, X = cuda(random_bf16((M, N), 111)), cuda(random_bf16((M, K), 112))
+    w1, b1 = B.enc_linear_bwd_weight(dY, X)
+    w2, b2 = B.enc_linear_bwd_weight(dY, X)
+    w0, b0 = B.enc_linear_bwd_weight(dY, X, split=False)
+    torch.cuda.synchronize()
+    assert torch.equal(w1, w2) and torch.equal(b1, b2)
+    rdW, rdb = oracle.linear_bwd_weight(f64(dY), f64(X))
+    for got in (w1, w0):
+        assert max_rel(f64(got), rdW) < 1e-5
+    for got in (b1, b0):
+        assert max_rel(f64(got), rdb) < 1e-5
+    # a workspace one byte short is refused before anything runs
+    need = B.linear_bwd_weight_workspace_bytes(M, N, K)
+    short = torch.empty(need - 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(B.EncError) as e:
+        B.enc_linear_bwd_weight(dY, X, ws=short)
+    assert e.value.status == B.ENC_ERR_WORKSPACE
 
 
 def test_named_weight_gradients_match_generic():

@@ -51,7 +51,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = B.lib()
-    assert L.enc_abi_version() == 1
+    assert L.enc_abi_version() == 2
     for code in (0, -1, -2, -3, -4, -5):
         assert len(L.enc_status_string(code)) > 0
     assert L.enc_status_string(7) == b"unknown status"
@@ -87,6 +87,23 @@ def test_parallel_saved_layout_is_aligned_and_disjoint(cfg):
     assert spans[-1][1] <= lay["total"]
     assert B.parallel_workspace_bytes(cfg) > 0
     assert B.qk_norm_bwd_workspace_bytes(M, nh, cfg["head_dim"]) % (4 * 4 * cfg["head_dim"]) == 0
+
+
+def test_weight_gradient_split_plan_sizes():
+    # outputs that fill the GPU never split; small outputs with many tokens do
+    assert B.linear_bwd_weight_workspace_bytes(2048, 24576, 6144) == 0
+    assert B.linear_bwd_weight_workspace_bytes(2048, 6144, 18432) == 0
+    assert B.linear_bwd_weight_workspace_bytes(394, 576, 192) == 0
+    # ViT-Base's out-projection: a 768 x 768 output over 6304 tokens; one fp32
+    # partial of dW and db per split, two or more splits
+    need = B.linear_bwd_weight_workspace_bytes(6304, 768, 768)
+    assert need % (768 * 768 * 4 + 768 * 4) == 0 and need // (768 * 768 * 4 + 768 * 4) >= 2
+    # the layer workspace holds the largest of the four weight gradients' partials
+    base = dict(batch=32, seq=197, hidden=768, heads=12, head_dim=64, mlp=3072, ln_eps=1e-6)
+    M = 32 * 197
+    wg = max(B.linear_bwd_weight_workspace_bytes(M, n, k) for n, k in ((768, 3072), (3072, 768), (768, 768),
+                                                                        (2304, 768)))
+    assert wg > 0 and B.layer_workspace_bytes(base) >= wg
 
 
 def test_workspace_sizes():
@@ -171,9 +188,16 @@ def test_null_and_misaligned_pointers_are_rejected():
         == B.ENC_ERR_UNSUPPORTED
     assert _status("enc_qkv_bwd_data_add", 8, 64, 64, p, p, z, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_attn_fwd", 1, 8, 1, 64, p, z, p, s) == B.ENC_ERR_INVALID
-    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, z, z, 0, s) == B.ENC_ERR_INVALID
+    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, z, z, 0, z, 0, s) == B.ENC_ERR_INVALID
     # db may be NULL, but a misaligned db is an error
-    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, p, ctypes.c_void_p(FAKE + 4), 0, s) == B.ENC_ERR_ALIGN
+    assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, p, ctypes.c_void_p(FAKE + 4), 0, z, 0, s) \
+        == B.ENC_ERR_ALIGN
+    # a workspace is optional, but a given one must be aligned and large enough
+    need = B.linear_bwd_weight_workspace_bytes(6304, 768, 768)
+    assert need > 0
+    assert _status("enc_linear_bwd_weight", 6304, 768, 768, p, p, p, p, 0, ctypes.c_void_p(FAKE + 8), need, s) \
+        == B.ENC_ERR_ALIGN
+    assert _status("enc_linear_bwd_weight", 6304, 768, 768, p, p, p, p, 0, p, need - 1, s) == B.ENC_ERR_WORKSPACE
 
 
 @no_gpu_only
