@@ -113,7 +113,7 @@ const char *enc_status_string(int status);
 /* Description of the last failure on the calling thread ("" if none). */
 const char *enc_last_error(void);
 /* ABI version of this header (bumped on incompatible change; 2: workspace
- * arguments of the weight-gradient entry points). */
+ * arguments of the projection entry points). */
 int enc_abi_version(void);
 
 /* ------------------------------------------------------------ sizing */
@@ -137,8 +137,9 @@ int enc_attn_bwd_workspace_bytes(int batch, int seq, int heads, int head_dim, si
  * the forward chain in order (LN1, QKV projection, attention, output
  * projection + residual, LN2, MLP up + GELU, MLP down + residual) on one
  * stream.  x, out: [M, H].  saved: enc_saved_layout().total bytes, filled
- * with the intermediates the backward needs.  ws: workspace of
- * enc_layer_workspace_bytes() bytes (ws_bytes states its size). */
+ * with the intermediates the backward needs.  ws: NULL (no product is
+ * split) or a workspace of enc_layer_workspace_bytes() bytes (ws_bytes
+ * states its size; the forward uses it for split-product partials). */
 int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params,
                       const enc_bf16 *x, enc_bf16 *out, void *saved,
                       void *ws, size_t ws_bytes, enc_stream_t stream);
@@ -152,6 +153,24 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params,
                       const enc_bf16 *dout, enc_bf16 *dx,
                       const enc_grads_t *grads, int accumulate,
                       void *ws, size_t ws_bytes, enc_stream_t stream);
+
+/* ------------------------------------------------------------ product workspaces
+ *
+ * Every projection entry point (forward, input gradient, weight gradient)
+ * takes an optional workspace `ws` of `ws_bytes` bytes.  With ws = NULL the
+ * product runs unsplit.  With a workspace of at least the size query's bytes,
+ * a product whose output tiles would leave most of the GPU idle splits its
+ * contraction over several workgroups per tile: fp32 partials go to ws and a
+ * second kernel adds them in a fixed order and applies the epilogue, so
+ * results stay deterministic for a given shape and workspace choice.  The
+ * queries return 0 for shapes that never split; a given workspace smaller
+ * than the query is ENC_ERR_WORKSPACE.  Forward and input-gradient products
+ * with output [M, N] and contraction K:
+ *   enc_qkv_fwd        (M, 3A, H)   enc_oproj_fwd       (M, H, A)
+ *   enc_mlp_up_fwd     (M, F, H)    enc_mlp_down_fwd    (M, H, F)
+ *   enc_mlp_down_bwd_data (M, F, H) enc_mlp_up_bwd_data (M, H, F)
+ *   enc_oproj_bwd_data (M, A, H)    enc_qkv_bwd_data[_add] (M, H, 3A) */
+int enc_linear_workspace_bytes(int M, int N, int K, size_t *bytes);
 
 /* ------------------------------------------------------------ forward kernels
  *
@@ -178,7 +197,8 @@ int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma,
  * QKV projection: qkv[M, 3A] = y1[M, H] * w_qkv[3A, H]^T + b_qkv[3A].
  * b_qkv may be NULL (no bias, as in the ViT-22B-style block below). */
 int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv,
-                const enc_bf16 *b_qkv, enc_bf16 *qkv, enc_stream_t stream);
+                const enc_bf16 *b_qkv, enc_bf16 *qkv, void *ws, size_t ws_bytes,
+                enc_stream_t stream);
 
 /* [Block step: multi-head self-attention (Appendix A heads x head dim; §3.1 decision 3)]
  * Bidirectional softmax attention of every (sequence, head): for queries i
@@ -195,22 +215,22 @@ int enc_attn_fwd(int batch, int seq, int heads, int head_dim,
  * w_o[H, A]^T + b_o[H]. */
 int enc_oproj_fwd(int M, int A, int H, const enc_bf16 *o, const enc_bf16 *w_o,
                   const enc_bf16 *b_o, const enc_bf16 *resid, enc_bf16 *h,
-                  enc_stream_t stream);
+                  void *ws, size_t ws_bytes, enc_stream_t stream);
 
 /* [Block step: MLP up-projection to the MLP dimension of Appendix A, GELU (§3.1 decision 3)]
  * MLP up-projection with GELU: u[M, F] = y2[M, H] * w_1[F, H]^T + b_1[F];
  * g = GELU(u) = u * Phi(u) (exact erf form).  Both u and g are written
  * (u is kept for the backward). */
 int enc_mlp_up_fwd(int M, int H, int F, const enc_bf16 *y2, const enc_bf16 *w_1,
-                   const enc_bf16 *b_1, enc_bf16 *u, enc_bf16 *g,
-                   enc_stream_t stream);
+                   const enc_bf16 *b_1, enc_bf16 *u, enc_bf16 *g, void *ws,
+                   size_t ws_bytes, enc_stream_t stream);
 
 /* [Block step: MLP down-projection + residual (§3.1 decision 3)]
  * MLP down-projection with residual: out[M, H] = resid[M, H] + g[M, F] *
  * w_2[H, F]^T + b_2[H]. */
 int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2,
                      const enc_bf16 *b_2, const enc_bf16 *resid, enc_bf16 *out,
-                     enc_stream_t stream);
+                     void *ws, size_t ws_bytes, enc_stream_t stream);
 
 /* ------------------------------------------------------------ backward kernels
  *
@@ -224,22 +244,25 @@ int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2
  * * GELU'(u), GELU'(u) = Phi(u) + u*phi(u); u is the saved pre-activation. */
 int enc_mlp_down_bwd_data(int M, int F, int H, const enc_bf16 *dout,
                           const enc_bf16 *w_2, const enc_bf16 *u, enc_bf16 *du,
-                          enc_stream_t stream);
+                          void *ws, size_t ws_bytes, enc_stream_t stream);
 
 /* [Backward of the MLP up-projection, input side (§3.1 decision 3; §4.2)]
  * MLP up input gradient: dy2[M, H] = du[M, F] * w_1[F, H]. */
 int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du,
-                        const enc_bf16 *w_1, enc_bf16 *dy2, enc_stream_t stream);
+                        const enc_bf16 *w_1, enc_bf16 *dy2, void *ws,
+                        size_t ws_bytes, enc_stream_t stream);
 
 /* [Backward of the output projection, input side (§3.1 decision 3; §4.2)]
  * Output projection input gradient: do_[M, A] = dh[M, H] * w_o[H, A]. */
 int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh,
-                       const enc_bf16 *w_o, enc_bf16 *do_, enc_stream_t stream);
+                       const enc_bf16 *w_o, enc_bf16 *do_, void *ws,
+                       size_t ws_bytes, enc_stream_t stream);
 
 /* [Backward of the QKV projection, input side (§3.1 decision 3; §4.2)]
  * QKV projection input gradient: dy1[M, H] = dqkv[M, 3A] * w_qkv[3A, H]. */
 int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv,
-                     const enc_bf16 *w_qkv, enc_bf16 *dy1, enc_stream_t stream);
+                     const enc_bf16 *w_qkv, enc_bf16 *dy1, void *ws,
+                     size_t ws_bytes, enc_stream_t stream);
 
 /* [Backward of the four projections, parameter side; fp32 gradients (§4.5)]
  * Parameter gradients of a linear layer Y = X W^T + b, summed over the M
@@ -377,7 +400,8 @@ int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params,
                          const enc_bf16 *x, enc_bf16 *out, void *saved,
                          enc_stream_t stream);
 
-/* Exact gradient of encoder_parallel_fwd.  dy of the shared LayerNorm is the
+/* (The block's two composites run every product unsplit.)
+ * Exact gradient of encoder_parallel_fwd.  dy of the shared LayerNorm is the
  * sum of both branches' input gradients (the QKV input gradient adds the
  * MLP branch's in its epilogue); dx = dout + LN backward(dy).  accumulate as
  * for encoder_layer_bwd; deterministic. */
@@ -417,7 +441,8 @@ int enc_qk_norm_bwd(int M, int heads, int head_dim, const enc_bf16 *dqkvn,
  * addend[M, H], accumulated in fp32 before one rounding to bf16. */
 int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv,
                          const enc_bf16 *w_qkv, const enc_bf16 *addend,
-                         enc_bf16 *dy, enc_stream_t stream);
+                         enc_bf16 *dy, void *ws, size_t ws_bytes,
+                         enc_stream_t stream);
 
 /* ------------------------------------------------------------ whole encoder
  *

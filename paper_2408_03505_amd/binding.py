@@ -77,15 +77,16 @@ _SIGS = {
     "encoder_layer_fwd": [_PCFG, ctypes.POINTER(EncParams), _p, _p, _p, _p, _sz, _p],
     "encoder_layer_bwd": [_PCFG, ctypes.POINTER(EncParams), _p, _p, _p, _p, ctypes.POINTER(EncGrads), _i, _p, _sz, _p],
     "enc_ln_fwd": [_i, _i, _p, _p, _p, _f, _p, _p, _p, _p],
-    "enc_qkv_fwd": [_i, _i, _i, _p, _p, _p, _p, _p],
+    "enc_qkv_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
     "enc_attn_fwd": [_i, _i, _i, _i, _p, _p, _p, _p],
-    "enc_oproj_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p],
-    "enc_mlp_up_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p],
-    "enc_mlp_down_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p],
-    "enc_mlp_down_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _p],
-    "enc_mlp_up_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
-    "enc_oproj_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
-    "enc_qkv_bwd_data": [_i, _i, _i, _p, _p, _p, _p],
+    "enc_oproj_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_mlp_up_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_mlp_down_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_mlp_down_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "enc_mlp_up_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _sz, _p],
+    "enc_oproj_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _sz, _p],
+    "enc_qkv_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _sz, _p],
+    "enc_linear_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
     "enc_linear_bwd_weight_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
     "enc_linear_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_mlp_down_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
@@ -105,7 +106,7 @@ _SIGS = {
     "enc_qk_norm_fwd": [_i, _i, _i, _p, _p, _p, _p, _p, _f, _p, _p, _p],
     "enc_qk_norm_bwd_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
     "enc_qk_norm_bwd": [_i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
-    "enc_qkv_bwd_data_add": [_i, _i, _i, _p, _p, _p, _p, _p],
+    "enc_qkv_bwd_data_add": [_i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
     "enc_patch_embed_workspace_bytes": [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
     "enc_patch_embed_fwd": [_i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p],
     "enc_patch_embed_bwd": [_i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _i, _p, _sz, _p],
@@ -249,8 +250,10 @@ def encoder_layer_fwd(cfg, params, x, out=None, saved=None, ws=None, stream=None
     total = saved_layout(cfg)["total"]
     saved = _out(saved, "saved", (total,), x, torch.uint8)
     c, p = make_cfg(cfg), _params_struct(cfg, params)
+    if ws is None:  # the layer workspace (split-product partials in the forward)
+        ws = torch.empty(layer_workspace_bytes(cfg), dtype=torch.uint8, device=x.device)
     _call("encoder_layer_fwd", ctypes.byref(c), ctypes.byref(p), _ptr(x), _ptr(out), _ptr(saved),
-          _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
+          _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
     return out, saved
 
 
@@ -293,7 +296,7 @@ def enc_ln_fwd(x, gamma, beta, eps, y=None, mean=None, rstd=None, stream=None):
     return y, mean, rstd
 
 
-def enc_qkv_fwd(y1, w_qkv, b_qkv, qkv=None, stream=None):
+def enc_qkv_fwd(y1, w_qkv, b_qkv, qkv=None, ws=None, split=True, stream=None):
     M, H = y1.shape
     A3 = w_qkv.shape[0]
     _check(y1, "y1", (M, H))
@@ -303,7 +306,8 @@ def enc_qkv_fwd(y1, w_qkv, b_qkv, qkv=None, stream=None):
     qkv = _out(qkv, "qkv", (M, A3), y1)
     if A3 % 3:
         raise ValueError("w_qkv rows must be 3*A")
-    _call("enc_qkv_fwd", M, H, A3 // 3, _ptr(y1), _ptr(w_qkv), _ptr(b_qkv), _ptr(qkv), _stream(stream))
+    wp, wn = _gemm_ws(M, A3, H, ws, split, y1.device)
+    _call("enc_qkv_fwd", M, H, A3 // 3, _ptr(y1), _ptr(w_qkv), _ptr(b_qkv), _ptr(qkv), wp, wn, _stream(stream))
     return qkv
 
 
@@ -316,7 +320,7 @@ def enc_attn_fwd(batch, seq, heads, head_dim, qkv, o=None, lse=None, stream=None
     return o, lse
 
 
-def enc_oproj_fwd(o, w_o, b_o, resid, h=None, stream=None):
+def enc_oproj_fwd(o, w_o, b_o, resid, h=None, ws=None, split=True, stream=None):
     M, A = o.shape
     H = w_o.shape[0]
     _check(o, "o", (M, A))
@@ -324,11 +328,12 @@ def enc_oproj_fwd(o, w_o, b_o, resid, h=None, stream=None):
     _check(b_o, "b_o", (H,))
     _check(resid, "resid", (M, H))
     h = _out(h, "h", (M, H), o)
-    _call("enc_oproj_fwd", M, A, H, _ptr(o), _ptr(w_o), _ptr(b_o), _ptr(resid), _ptr(h), _stream(stream))
+    wp, wn = _gemm_ws(M, H, A, ws, split, o.device)
+    _call("enc_oproj_fwd", M, A, H, _ptr(o), _ptr(w_o), _ptr(b_o), _ptr(resid), _ptr(h), wp, wn, _stream(stream))
     return h
 
 
-def enc_mlp_up_fwd(y2, w_1, b_1, u=None, g=None, stream=None):
+def enc_mlp_up_fwd(y2, w_1, b_1, u=None, g=None, ws=None, split=True, stream=None):
     M, H = y2.shape
     F = w_1.shape[0]
     _check(y2, "y2", (M, H))
@@ -336,11 +341,12 @@ def enc_mlp_up_fwd(y2, w_1, b_1, u=None, g=None, stream=None):
     _check(b_1, "b_1", (F,))
     u = _out(u, "u", (M, F), y2)
     g = _out(g, "g", (M, F), y2)
-    _call("enc_mlp_up_fwd", M, H, F, _ptr(y2), _ptr(w_1), _ptr(b_1), _ptr(u), _ptr(g), _stream(stream))
+    wp, wn = _gemm_ws(M, F, H, ws, split, y2.device)
+    _call("enc_mlp_up_fwd", M, H, F, _ptr(y2), _ptr(w_1), _ptr(b_1), _ptr(u), _ptr(g), wp, wn, _stream(stream))
     return u, g
 
 
-def enc_mlp_down_fwd(g, w_2, b_2, resid, out=None, stream=None):
+def enc_mlp_down_fwd(g, w_2, b_2, resid, out=None, ws=None, split=True, stream=None):
     M, F = g.shape
     H = w_2.shape[0]
     _check(g, "g", (M, F))
@@ -348,50 +354,56 @@ def enc_mlp_down_fwd(g, w_2, b_2, resid, out=None, stream=None):
     _check(b_2, "b_2", (H,))
     _check(resid, "resid", (M, H))
     out = _out(out, "out", (M, H), g)
-    _call("enc_mlp_down_fwd", M, F, H, _ptr(g), _ptr(w_2), _ptr(b_2), _ptr(resid), _ptr(out), _stream(stream))
+    wp, wn = _gemm_ws(M, H, F, ws, split, g.device)
+    _call("enc_mlp_down_fwd", M, F, H, _ptr(g), _ptr(w_2), _ptr(b_2), _ptr(resid), _ptr(out), wp, wn,
+          _stream(stream))
     return out
 
 
 # ------------------------------------------------------------------ backward kernels
 
-def enc_mlp_down_bwd_data(dout, w_2, u, du=None, stream=None):
+def enc_mlp_down_bwd_data(dout, w_2, u, du=None, ws=None, split=True, stream=None):
     M, H = dout.shape
     F = w_2.shape[1]
     _check(dout, "dout", (M, H))
     _check(w_2, "w_2", (H, F))
     _check(u, "u", (M, F))
     du = _out(du, "du", (M, F), dout)
-    _call("enc_mlp_down_bwd_data", M, F, H, _ptr(dout), _ptr(w_2), _ptr(u), _ptr(du), _stream(stream))
+    wp, wn = _gemm_ws(M, F, H, ws, split, dout.device)
+    _call("enc_mlp_down_bwd_data", M, F, H, _ptr(dout), _ptr(w_2), _ptr(u), _ptr(du), wp, wn, _stream(stream))
     return du
 
 
-def enc_mlp_up_bwd_data(du, w_1, dy2=None, stream=None):
+def enc_mlp_up_bwd_data(du, w_1, dy2=None, ws=None, split=True, stream=None):
     M, F = du.shape
     H = w_1.shape[1]
     _check(du, "du", (M, F))
     _check(w_1, "w_1", (F, H))
     dy2 = _out(dy2, "dy2", (M, H), du)
-    _call("enc_mlp_up_bwd_data", M, H, F, _ptr(du), _ptr(w_1), _ptr(dy2), _stream(stream))
+    wp, wn = _gemm_ws(M, H, F, ws, split, du.device)
+    _call("enc_mlp_up_bwd_data", M, H, F, _ptr(du), _ptr(w_1), _ptr(dy2), wp, wn, _stream(stream))
     return dy2
 
 
-def enc_oproj_bwd_data(dh, w_o, do=None, stream=None):
+def enc_oproj_bwd_data(dh, w_o, do=None, ws=None, split=True, stream=None):
     M, H = dh.shape
     A = w_o.shape[1]
     _check(dh, "dh", (M, H))
     _check(w_o, "w_o", (H, A))
     do = _out(do, "do", (M, A), dh)
-    _call("enc_oproj_bwd_data", M, A, H, _ptr(dh), _ptr(w_o), _ptr(do), _stream(stream))
+    wp, wn = _gemm_ws(M, A, H, ws, split, dh.device)
+    _call("enc_oproj_bwd_data", M, A, H, _ptr(dh), _ptr(w_o), _ptr(do), wp, wn, _stream(stream))
     return do
 
 
-def enc_qkv_bwd_data(dqkv, w_qkv, dy1=None, stream=None):
+def enc_qkv_bwd_data(dqkv, w_qkv, dy1=None, ws=None, split=True, stream=None):
     M, A3 = dqkv.shape
     H = w_qkv.shape[1]
     _check(dqkv, "dqkv", (M, A3))
     _check(w_qkv, "w_qkv", (A3, H))
     dy1 = _out(dy1, "dy1", (M, H), dqkv)
-    _call("enc_qkv_bwd_data", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(dy1), _stream(stream))
+    wp, wn = _gemm_ws(M, H, A3, ws, split, dqkv.device)
+    _call("enc_qkv_bwd_data", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(dy1), wp, wn, _stream(stream))
     return dy1
 
 
@@ -399,6 +411,26 @@ def linear_bwd_weight_workspace_bytes(M, N, K):
     n = _sz()
     _call("enc_linear_bwd_weight_workspace_bytes", M, N, K, ctypes.byref(n))
     return n.value
+
+
+def linear_workspace_bytes(M, N, K):
+    n = _sz()
+    _call("enc_linear_workspace_bytes", M, N, K, ctypes.byref(n))
+    return n.value
+
+
+def _gemm_ws(M, N, K, ws, split, device):
+    """Workspace argument of a forward or input-gradient product with output
+    [M, N] and contraction K: a caller tensor, a fresh one of the queried
+    size (split=True, ws=None), or none (split=False)."""
+    if not split:
+        return ctypes.c_void_p(0), 0
+    if ws is None:
+        need = linear_workspace_bytes(M, N, K)
+        if need == 0:
+            return ctypes.c_void_p(0), 0
+        ws = torch.empty(need, dtype=torch.uint8, device=device)
+    return _ptr(ws), ws.numel() * ws.element_size()
 
 
 def _wgrad_ws(M, N, K, ws, split, device):
@@ -705,14 +737,16 @@ def enc_qk_norm_bwd(heads, head_dim, dqkvn, qkv, stats, qn_g, kn_g, dqkv=None, g
     return dqkv, grads
 
 
-def enc_qkv_bwd_data_add(dqkv, w_qkv, addend, dy=None, stream=None):
+def enc_qkv_bwd_data_add(dqkv, w_qkv, addend, dy=None, ws=None, split=True, stream=None):
     M, A3 = dqkv.shape
     H = w_qkv.shape[1]
     _check(dqkv, "dqkv", (M, A3))
     _check(w_qkv, "w_qkv", (A3, H))
     _check(addend, "addend", (M, H))
     dy = _out(dy, "dy", (M, H), dqkv)
-    _call("enc_qkv_bwd_data_add", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(addend), _ptr(dy), _stream(stream))
+    wp, wn = _gemm_ws(M, H, A3, ws, split, dqkv.device)
+    _call("enc_qkv_bwd_data_add", M, H, A3 // 3, _ptr(dqkv), _ptr(w_qkv), _ptr(addend), _ptr(dy), wp, wn,
+          _stream(stream))
     return dy
 
 

@@ -155,11 +155,20 @@ struct BwdWs {
   size_t du, dy2, dh, dO, dqkv, dy1, ln_part, dvec, wg, wg_bytes, total;
 };
 
-// Workspace of the four weight gradients of a layer (each uses it in turn).
-size_t layer_wgrad_ws(const enc_cfg_t *c) {
+// Partial sums of the layer's split products (each GEMM uses the region in
+// turn): the largest need of the four weight gradients, the four input
+// gradients and the four forward projections.
+size_t layer_gemm_ws(const enc_cfg_t *c) {
   const int M = c->batch * c->seq, H = c->hidden, A = c->heads * c->head_dim, F = c->mlp;
-  return std::max(std::max(gemm_wgrad_ws_bytes(H, F, M), gemm_wgrad_ws_bytes(F, H, M)),
-                  std::max(gemm_wgrad_ws_bytes(H, A, M), gemm_wgrad_ws_bytes(3 * A, H, M)));
+  const size_t wg = std::max(std::max(gemm_wgrad_ws_bytes(H, F, M), gemm_wgrad_ws_bytes(F, H, M)),
+                             std::max(gemm_wgrad_ws_bytes(H, A, M), gemm_wgrad_ws_bytes(3 * A, H, M)));
+  // input gradients: du [M, F] over H, dy2 [M, H] over F, dO [M, A] over H, dy1 [M, H] over 3A
+  const size_t dg = std::max(std::max(gemm_ws_bytes(M, F, H), gemm_ws_bytes(M, H, F)),
+                             std::max(gemm_ws_bytes(M, A, H), gemm_ws_bytes(M, H, 3 * A)));
+  // forward: qkv [M, 3A] over H, h [M, H] over A, u [M, F] over H, out [M, H] over F
+  const size_t fw = std::max(std::max(gemm_ws_bytes(M, 3 * A, H), gemm_ws_bytes(M, H, A)),
+                             std::max(gemm_ws_bytes(M, F, H), gemm_ws_bytes(M, H, F)));
+  return std::max(wg, std::max(dg, fw));
 }
 
 BwdWs bwd_layout(const enc_cfg_t *c) {
@@ -180,7 +189,7 @@ BwdWs bwd_layout(const enc_cfg_t *c) {
   w.dy1 = take(M * H * 2);
   w.ln_part = take(ln_bwd_ws_bytes(static_cast<int>(M), c->hidden));
   w.dvec = take(attn_bwd_ws_bytes(c->batch, c->seq, c->heads));
-  w.wg_bytes = layer_wgrad_ws(c);
+  w.wg_bytes = layer_gemm_ws(c);
   w.wg = take(w.wg_bytes);
   w.total = off;
   return w;
@@ -216,31 +225,32 @@ int check_grads(const char *fn, const enc_grads_t *g) {
 // ---- unchecked launch helpers shared by the per-kernel entry points and the chains
 
 bool gemm_fwd(int M, int N, int K, const bf16_t *X, const bf16_t *W, const bf16_t *bias, const bf16_t *R, bf16_t *Y,
-              bf16_t *Y2, Epi epi, hipStream_t s) {
+              bf16_t *Y2, Epi epi, void *ws, size_t ws_bytes, hipStream_t s) {
   GemmArgs a{};
   a.M = M, a.N = N, a.K = K;
   a.A = X, a.lda = K, a.B = W, a.ldb = K;
   a.Y = Y, a.ldy = N, a.bias = bias, a.R = R, a.Y2 = Y2;
-  return launch_gemm_fwd(a, epi, s);
+  return launch_gemm_fwd(a, epi, ws, ws_bytes, s);
 }
 
 // dX[M, K] = dY[M, N] * W[N, K]  (optionally times GELU'(U[M, K]))
-bool gemm_dgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *U, bf16_t *dX, hipStream_t s) {
+bool gemm_dgrad(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *U, bf16_t *dX, void *ws,
+                size_t ws_bytes, hipStream_t s) {
   GemmArgs a{};
   a.M = M, a.N = K, a.K = N;
   a.A = dY, a.lda = N, a.B = W, a.ldb = K;
   a.Y = dX, a.ldy = K, a.R = U;
-  return launch_gemm_dgrad(a, U ? Epi::kGeluGrad : Epi::kPlain, s);
+  return launch_gemm_dgrad(a, U ? Epi::kGeluGrad : Epi::kPlain, ws, ws_bytes, s);
 }
 
 // dX[M, K] = dY[M, N] * W[N, K] + R[M, K]
-bool gemm_dgrad_add(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *R, bf16_t *dX,
-                    hipStream_t s) {
+bool gemm_dgrad_add(int M, int N, int K, const bf16_t *dY, const bf16_t *W, const bf16_t *R, bf16_t *dX, void *ws,
+                    size_t ws_bytes, hipStream_t s) {
   GemmArgs a{};
   a.M = M, a.N = K, a.K = N;
   a.A = dY, a.lda = N, a.B = W, a.ldb = K;
   a.Y = dX, a.ldy = K, a.R = R;
-  return launch_gemm_dgrad(a, Epi::kResid, s);
+  return launch_gemm_dgrad(a, Epi::kResid, ws, ws_bytes, s);
 }
 
 // dW[N, K] (+)= dY[M, N]^T X[M, K]; db[N] (+)= sum_m dY
@@ -262,6 +272,16 @@ int linear_dims(const char *fn, int M, std::initializer_list<int> feats) {
     if (f % 8) return fail(ENC_ERR_UNSUPPORTED, "%s: feature widths must be multiples of 8 (got %d)", fn, f);
   for (int f : feats)
     if (static_cast<long>(M) * f >= kMaxElems) return fail(ENC_ERR_UNSUPPORTED, "%s: tensor exceeds 2^31 elements", fn);
+  return ENC_OK;
+}
+
+// An optional product workspace: NULL, or 16-byte aligned and at least the
+// size query's bytes for output [M, N] and contraction K.
+int check_gemm_ws(const char *fn, const void *ws, size_t ws_bytes, int M, int N, int K) {
+  if (!ws) return ENC_OK;
+  if (!aligned16(ws)) return fail(ENC_ERR_ALIGN, "%s: ws is not 16-byte aligned", fn);
+  const size_t need = gemm_ws_bytes(M, N, K);
+  if (ws_bytes < need) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, need);
   return ENC_OK;
 }
 
@@ -473,16 +493,17 @@ int enc_ln_fwd(int rows, int cols, const enc_bf16 *x, const enc_bf16 *gamma, con
 }
 
 int enc_qkv_fwd(int M, int H, int A, const enc_bf16 *y1, const enc_bf16 *w_qkv, const enc_bf16 *b_qkv, enc_bf16 *qkv,
-                enc_stream_t stream) {
+                void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_qkv_fwd";
   int r = linear_dims(fn, M, {H, A, 3 * A});
   if (r) return r;
   PtrCheck c(fn);
   c.req(y1, "y1").req(w_qkv, "w_qkv").opt(b_qkv, "b_qkv").req(qkv, "qkv");
   if (c.code) return c.code;
-  if (!gemm_fwd(M, 3 * A, H, y1, w_qkv, b_qkv, nullptr, qkv, nullptr, b_qkv ? Epi::kBias : Epi::kPlain,
-                as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, 3 * A, H))) return r;
+  if (!gemm_fwd(M, 3 * A, H, y1, w_qkv, b_qkv, nullptr, qkv, nullptr, b_qkv ? Epi::kBias : Epi::kPlain, ws,
+                ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
@@ -500,106 +521,123 @@ int enc_attn_fwd(int batch, int seq, int heads, int head_dim, const enc_bf16 *qk
 }
 
 int enc_oproj_fwd(int M, int A, int H, const enc_bf16 *o, const enc_bf16 *w_o, const enc_bf16 *b_o,
-                  const enc_bf16 *resid, enc_bf16 *h, enc_stream_t stream) {
+                  const enc_bf16 *resid, enc_bf16 *h, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_oproj_fwd";
   int r = linear_dims(fn, M, {H, A});
   if (r) return r;
   PtrCheck c(fn);
   c.req(o, "o").req(w_o, "w_o").req(b_o, "b_o").req(resid, "resid").req(h, "h");
   if (c.code) return c.code;
-  if (!gemm_fwd(M, H, A, o, w_o, b_o, resid, h, nullptr, Epi::kBiasResid, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, H, A))) return r;
+  if (!gemm_fwd(M, H, A, o, w_o, b_o, resid, h, nullptr, Epi::kBiasResid, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
 int enc_mlp_up_fwd(int M, int H, int F, const enc_bf16 *y2, const enc_bf16 *w_1, const enc_bf16 *b_1, enc_bf16 *u,
-                   enc_bf16 *g, enc_stream_t stream) {
+                   enc_bf16 *g, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_mlp_up_fwd";
   int r = linear_dims(fn, M, {H, F});
   if (r) return r;
   PtrCheck c(fn);
   c.req(y2, "y2").req(w_1, "w_1").req(b_1, "b_1").req(u, "u").req(g, "g");
   if (c.code) return c.code;
-  if (!gemm_fwd(M, F, H, y2, w_1, b_1, nullptr, u, g, Epi::kBiasGelu, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, F, H))) return r;
+  if (!gemm_fwd(M, F, H, y2, w_1, b_1, nullptr, u, g, Epi::kBiasGelu, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
 int enc_mlp_down_fwd(int M, int F, int H, const enc_bf16 *g, const enc_bf16 *w_2, const enc_bf16 *b_2,
-                     const enc_bf16 *resid, enc_bf16 *out, enc_stream_t stream) {
+                     const enc_bf16 *resid, enc_bf16 *out, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_mlp_down_fwd";
   int r = linear_dims(fn, M, {H, F});
   if (r) return r;
   PtrCheck c(fn);
   c.req(g, "g").req(w_2, "w_2").req(b_2, "b_2").req(resid, "resid").req(out, "out");
   if (c.code) return c.code;
-  if (!gemm_fwd(M, H, F, g, w_2, b_2, resid, out, nullptr, Epi::kBiasResid, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, H, F))) return r;
+  if (!gemm_fwd(M, H, F, g, w_2, b_2, resid, out, nullptr, Epi::kBiasResid, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
 // ------------------------------------------------------------ backward kernels
 
 int enc_mlp_down_bwd_data(int M, int F, int H, const enc_bf16 *dout, const enc_bf16 *w_2, const enc_bf16 *u,
-                          enc_bf16 *du, enc_stream_t stream) {
+                          enc_bf16 *du, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_mlp_down_bwd_data";
   int r = linear_dims(fn, M, {H, F});
   if (r) return r;
   PtrCheck c(fn);
   c.req(dout, "dout").req(w_2, "w_2").req(u, "u").req(du, "du");
   if (c.code) return c.code;
-  if (!gemm_dgrad(M, H, F, dout, w_2, u, du, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, F, H))) return r;
+  if (!gemm_dgrad(M, H, F, dout, w_2, u, du, ws, ws_bytes, as_stream(stream))) return refused_after_checks(fn);
   return launched(fn);
 }
 
-int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du, const enc_bf16 *w_1, enc_bf16 *dy2,
-                        enc_stream_t stream) {
+int enc_mlp_up_bwd_data(int M, int H, int F, const enc_bf16 *du, const enc_bf16 *w_1, enc_bf16 *dy2, void *ws,
+                        size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_mlp_up_bwd_data";
   int r = linear_dims(fn, M, {H, F});
   if (r) return r;
   PtrCheck c(fn);
   c.req(du, "du").req(w_1, "w_1").req(dy2, "dy2");
   if (c.code) return c.code;
-  if (!gemm_dgrad(M, F, H, du, w_1, nullptr, dy2, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, H, F))) return r;
+  if (!gemm_dgrad(M, F, H, du, w_1, nullptr, dy2, ws, ws_bytes, as_stream(stream))) return refused_after_checks(fn);
   return launched(fn);
 }
 
-int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh, const enc_bf16 *w_o, enc_bf16 *do_,
-                       enc_stream_t stream) {
+int enc_oproj_bwd_data(int M, int A, int H, const enc_bf16 *dh, const enc_bf16 *w_o, enc_bf16 *do_, void *ws,
+                       size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_oproj_bwd_data";
   int r = linear_dims(fn, M, {H, A});
   if (r) return r;
   PtrCheck c(fn);
   c.req(dh, "dh").req(w_o, "w_o").req(do_, "do");
   if (c.code) return c.code;
-  if (!gemm_dgrad(M, H, A, dh, w_o, nullptr, do_, as_stream(stream))) return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, A, H))) return r;
+  if (!gemm_dgrad(M, H, A, dh, w_o, nullptr, do_, ws, ws_bytes, as_stream(stream))) return refused_after_checks(fn);
   return launched(fn);
 }
 
-int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *w_qkv, enc_bf16 *dy1,
-                     enc_stream_t stream) {
+int enc_qkv_bwd_data(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *w_qkv, enc_bf16 *dy1, void *ws,
+                     size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_qkv_bwd_data";
   int r = linear_dims(fn, M, {H, A, 3 * A});
   if (r) return r;
   PtrCheck c(fn);
   c.req(dqkv, "dqkv").req(w_qkv, "w_qkv").req(dy1, "dy1");
   if (c.code) return c.code;
-  if (!gemm_dgrad(M, 3 * A, H, dqkv, w_qkv, nullptr, dy1, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, H, 3 * A))) return r;
+  if (!gemm_dgrad(M, 3 * A, H, dqkv, w_qkv, nullptr, dy1, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
 }
 
 int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv, const enc_bf16 *w_qkv, const enc_bf16 *addend,
-                         enc_bf16 *dy, enc_stream_t stream) {
+                         enc_bf16 *dy, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_qkv_bwd_data_add";
   int r = linear_dims(fn, M, {H, A, 3 * A});
   if (r) return r;
   PtrCheck c(fn);
   c.req(dqkv, "dqkv").req(w_qkv, "w_qkv").req(addend, "addend").req(dy, "dy");
   if (c.code) return c.code;
-  if (!gemm_dgrad_add(M, 3 * A, H, dqkv, w_qkv, addend, dy, as_stream(stream)))
-    return fail(ENC_ERR_UNSUPPORTED, "%s: no kernel", fn);
+  if ((r = check_gemm_ws(fn, ws, ws_bytes, M, H, 3 * A))) return r;
+  if (!gemm_dgrad_add(M, 3 * A, H, dqkv, w_qkv, addend, dy, ws, ws_bytes, as_stream(stream)))
+    return refused_after_checks(fn);
   return launched(fn);
+}
+
+int enc_linear_workspace_bytes(int M, int N, int K, size_t *bytes) {
+  const char *fn = "enc_linear_workspace_bytes";
+  int r = linear_dims(fn, M, {N, K});
+  if (r) return r;
+  if (!bytes) return fail(ENC_ERR_INVALID, "%s: bytes is NULL", fn);
+  *bytes = gemm_ws_bytes(M, N, K);
+  return ok();
 }
 
 int enc_linear_bwd_weight_workspace_bytes(int M, int N, int K, size_t *bytes) {
@@ -716,8 +754,10 @@ int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   PtrCheck c(fn);
   c.req(x, "x").req(out, "out").req(saved, "saved").opt(ws, "ws");
   if (c.code) return c.code;
-  (void)ws;
-  (void)ws_bytes;  // the forward chain needs no workspace beyond `saved`
+  // the workspace only holds split-product partials here (ws = NULL: no split)
+  const size_t gneed = layer_gemm_ws(cfg);
+  if (ws && ws_bytes < gneed) return fail(ENC_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, ws_bytes, gneed);
+  void *gp = ws && gneed ? ws : nullptr;
   enc_saved_layout_t L;
   saved_layout(cfg, &L);
   const int M = cfg->batch * cfg->seq, H = cfg->hidden, F = cfg->mlp, A = cfg->heads * cfg->head_dim;
@@ -730,12 +770,12 @@ int encoder_layer_fwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   float *mean2 = at<float>(saved, L.mean2), *rstd2 = at<float>(saved, L.rstd2);
 
   bool okk = launch_ln_fwd(M, H, x, p.ln1_g, p.ln1_b, cfg->ln_eps, y1, mean1, rstd1, s);
-  okk = okk && gemm_fwd(M, 3 * A, H, y1, p.w_qkv, p.b_qkv, nullptr, qkv, nullptr, Epi::kBias, s);
+  okk = okk && gemm_fwd(M, 3 * A, H, y1, p.w_qkv, p.b_qkv, nullptr, qkv, nullptr, Epi::kBias, gp, gneed, s);
   okk = okk && launch_attn_fwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkv, o, lse, s);
-  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, s);
+  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, gp, gneed, s);
   okk = okk && launch_ln_fwd(M, H, h, p.ln2_g, p.ln2_b, cfg->ln_eps, y2, mean2, rstd2, s);
-  okk = okk && gemm_fwd(M, F, H, y2, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);
-  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);
+  okk = okk && gemm_fwd(M, F, H, y2, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, gp, gneed, s);
+  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, gp, gneed, s);
   if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
@@ -770,15 +810,15 @@ int encoder_layer_bwd(const enc_cfg_t *cfg, const enc_params_t *params, const en
   float *part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec);
   void *wg = W.wg_bytes ? at<char>(ws, W.wg) : nullptr;  // split weight-gradient partials
 
-  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                      // du = dout W2 * GELU'(u)
+  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, wg, W.wg_bytes, s);      // du = dout W2 * GELU'(u)
   okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, wg, W.wg_bytes, s);          // dW2, db2
-  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy2, s);               // dy2 = du W1
+  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy2, wg, W.wg_bytes, s);  // dy2 = du W1
   okk = okk && gemm_wgrad(M, F, H, du, y2, gr.w_1, gr.b_1, acc, wg, W.wg_bytes, s);           // dW1, db1
   okk = okk && launch_ln_bwd(M, H, dy2, h, mean2, rstd2, p.ln2_g, dout, dh, gr.ln2_g, gr.ln2_b, acc, part, s);
-  okk = okk && gemm_dgrad(M, H, A, dh, p.w_o, nullptr, dO, s);                // dO = dh Wo
+  okk = okk && gemm_dgrad(M, H, A, dh, p.w_o, nullptr, dO, wg, W.wg_bytes, s);   // dO = dh Wo
   okk = okk && gemm_wgrad(M, H, A, dh, o, gr.w_o, gr.b_o, acc, wg, W.wg_bytes, s);            // dWo, dbo
   okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkv, o, lse, dO, dqkv, dvec, s);
-  okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, s);       // dy1 = dqkv Wqkv
+  okk = okk && gemm_dgrad(M, 3 * A, H, dqkv, p.w_qkv, nullptr, dy1, wg, W.wg_bytes, s);  // dy1 = dqkv Wqkv
   okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y1, gr.w_qkv, gr.b_qkv, acc, wg, W.wg_bytes, s);  // dWqkv, dbqkv
   okk = okk && launch_ln_bwd(M, H, dy1, x, mean1, rstd1, p.ln1_g, dh, dx, gr.ln1_g, gr.ln1_b, acc, part, s);
   if (!okk) return refused_after_checks(fn);
@@ -867,13 +907,13 @@ int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   float *qks = at<float>(saved, L.qkstats);
 
   bool okk = launch_ln_fwd(M, H, x, p.ln_g, p.ln_b, cfg->ln_eps, y, mean, rstd, s);
-  okk = okk && gemm_fwd(M, 3 * A, H, y, p.w_qkv, nullptr, nullptr, qkv, nullptr, Epi::kPlain, s);
+  okk = okk && gemm_fwd(M, 3 * A, H, y, p.w_qkv, nullptr, nullptr, qkv, nullptr, Epi::kPlain, nullptr, 0, s);
   okk = okk && launch_qk_norm_fwd(M, cfg->heads, cfg->head_dim, qkv, p.qn_g, p.qn_b, p.kn_g, p.kn_b, cfg->ln_eps,
                                   qkvn, qks, s);
   okk = okk && launch_attn_fwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkvn, o, lse, s);
-  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, s);   // x + attention branch
-  okk = okk && gemm_fwd(M, F, H, y, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, s);    // MLP reads y too
-  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, s);  // + MLP branch
+  okk = okk && gemm_fwd(M, H, A, o, p.w_o, p.b_o, x, h, nullptr, Epi::kBiasResid, nullptr, 0, s);  // + attention
+  okk = okk && gemm_fwd(M, F, H, y, p.w_1, p.b_1, nullptr, u, g, Epi::kBiasGelu, nullptr, 0, s);  // MLP reads y
+  okk = okk && gemm_fwd(M, H, F, g, p.w_2, p.b_2, h, out, nullptr, Epi::kBiasResid, nullptr, 0, s);  // + MLP
   if (!okk) return refused_after_checks(fn);
   return launched(fn);
 }
@@ -906,17 +946,17 @@ int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params, cons
   bf16_t *dqkvn = at<bf16_t>(ws, W.dqkvn), *dqkv = at<bf16_t>(ws, W.dqkv), *dy = at<bf16_t>(ws, W.dy);
   float *ln_part = at<float>(ws, W.ln_part), *dvec = at<float>(ws, W.dvec), *qk_part = at<float>(ws, W.qk_part);
 
-  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, s);                  // du = dout W2 * GELU'(u)
+  bool okk = gemm_dgrad(M, H, F, dout, p.w_2, u, du, nullptr, 0, s);      // du = dout W2 * GELU'(u)
   okk = okk && gemm_wgrad(M, H, F, dout, g, gr.w_2, gr.b_2, acc, nullptr, 0, s);      // dW2, db2
-  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy_mlp, s);        // MLP branch's dy
+  okk = okk && gemm_dgrad(M, F, H, du, p.w_1, nullptr, dy_mlp, nullptr, 0, s);  // MLP branch's dy
   okk = okk && gemm_wgrad(M, F, H, du, y, gr.w_1, gr.b_1, acc, nullptr, 0, s);        // dW1, db1
-  okk = okk && gemm_dgrad(M, H, A, dout, p.w_o, nullptr, dO, s);          // dO = dout Wo
+  okk = okk && gemm_dgrad(M, H, A, dout, p.w_o, nullptr, dO, nullptr, 0, s);  // dO = dout Wo
   okk = okk && gemm_wgrad(M, H, A, dout, o, gr.w_o, gr.b_o, acc, nullptr, 0, s);      // dWo, dbo
   okk = okk && launch_attn_bwd(cfg->batch, cfg->seq, cfg->heads, cfg->head_dim, qkvn, o, lse, dO, dqkvn, dvec, s);
   okk = okk && launch_qk_norm_bwd(M, cfg->heads, cfg->head_dim, dqkvn, qkv, qks, p.qn_g, p.kn_g, dqkv, gr.qn_g,
                                   gr.qn_b, gr.kn_g, gr.kn_b, acc, qk_part, s);
   okk = okk && gemm_wgrad(M, 3 * A, H, dqkv, y, gr.w_qkv, nullptr, acc, nullptr, 0, s);  // dWqkv (no bias)
-  okk = okk && gemm_dgrad_add(M, 3 * A, H, dqkv, p.w_qkv, dy_mlp, dy, s);   // dy = dqkv Wqkv + dy_mlp
+  okk = okk && gemm_dgrad_add(M, 3 * A, H, dqkv, p.w_qkv, dy_mlp, dy, nullptr, 0, s);  // + dy_mlp
   okk = okk && launch_ln_bwd(M, H, dy, x, mean, rstd, p.ln_g, dout, dx, gr.ln_g, gr.ln_b, acc, ln_part, s);
   if (!okk) return refused_after_checks(fn);
   return launched(fn);
@@ -952,7 +992,8 @@ int enc_patch_embed_fwd(int batch, int channels, int img_h, int img_w, int patch
   const hipStream_t s = as_stream(stream);
   bf16_t *tok = has_cls ? static_cast<bf16_t *>(ws) : x0;  // without a class token the tokens are x0's rows
   bool okk = launch_patchify(batch, channels, img_h, img_w, patch, Kp, images, patches, s);
-  okk = okk && gemm_fwd(batch * N, hidden, Kp, patches, w_pe, b_pe, nullptr, tok, nullptr, Epi::kBias, s);
+  okk = okk && gemm_fwd(batch * N, hidden, Kp, patches, w_pe, b_pe, nullptr, tok, nullptr, Epi::kBias, nullptr, 0,
+                        s);
   okk = okk && launch_patch_assemble(batch, N, S, hidden, has_cls, tok, cls, pos, x0, s);
   if (!okk) return refused_after_checks(fn);
   return launched(fn);

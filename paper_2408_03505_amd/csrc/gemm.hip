@@ -1076,28 +1076,117 @@ bool launch_lds(const GemmArgs &a, hipStream_t s) {
 
 }  // namespace
 
-bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s) {
+namespace {
+
+// Sum of the fp32 partials [S][M][N] in split order, then the epilogue of
+// the unsplit kernel: bias, residual, GELU (writing u and g) or GELU' (from
+// the saved u in R), rounded once to bf16.  Eight outputs per thread and
+// iteration (N is a multiple of 8).
+template <Epi EPI>
+__global__ __launch_bounds__(256) void splitk_epilogue_kernel(const float *__restrict__ part, int splits,
+                                                              size_t stride, int M, int N,
+                                                              const bf16_t *__restrict__ bias,
+                                                              const bf16_t *__restrict__ R, bf16_t *__restrict__ Y,
+                                                              bf16_t *__restrict__ Y2) {
+  const long n8 = static_cast<long>(M) * N / 8;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n8; i += static_cast<long>(gridDim.x) * 256) {
+    const size_t e0 = static_cast<size_t>(i) * 8;
+    f32x4_t lo = *reinterpret_cast<const f32x4_t *>(part + e0);
+    f32x4_t hi = *reinterpret_cast<const f32x4_t *>(part + e0 + 4);
+    for (int sp = 1; sp < splits; ++sp) {
+      lo += *reinterpret_cast<const f32x4_t *>(part + sp * stride + e0);
+      hi += *reinterpret_cast<const f32x4_t *>(part + sp * stride + e0 + 4);
+    }
+    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    if constexpr (EPI == Epi::kBias || EPI == Epi::kBiasResid || EPI == Epi::kBiasGelu) {
+      const u32x4_t bw = ldg16(bias + e0 % N);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] += lo_bf(bw[e]);
+        v[2 * e + 1] += hi_bf(bw[e]);
+      }
+    }
+    if constexpr (EPI == Epi::kBiasResid || EPI == Epi::kResid) {
+      const u32x4_t rw = ldg16(R + e0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] += lo_bf(rw[e]);
+        v[2 * e + 1] += hi_bf(rw[e]);
+      }
+    }
+    if constexpr (EPI == Epi::kGeluGrad) {
+      const u32x4_t uw = ldg16(R + e0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] *= gelu_grad_f(lo_bf(uw[e]));
+        v[2 * e + 1] *= gelu_grad_f(hi_bf(uw[e]));
+      }
+    }
+    u32x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = pack2(v[2 * e], v[2 * e + 1]);
+    stg16_nt(Y + e0, o);
+    if constexpr (EPI == Epi::kBiasGelu) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = pack2(gelu_f(v[2 * e]), gelu_f(v[2 * e + 1]));
+      stg16_nt(Y2 + e0, o);
+    }
+  }
+}
+
+// Split launch of a forward (AT = false, BT = false) or input-gradient
+// (BT = true) product: fp32 partials into ws, then the epilogue kernel.
+// Returns false (nothing launched) when the plan does not split or ws is
+// missing or too small.
+template <bool BT, Epi EPI>
+bool launch_split(const GemmArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
+  const SplitPlan sp = gemm_split_plan(a.M, a.N, a.K);
+  if (sp.splits <= 1 || ws == nullptr || ws_bytes < gemm_ws_bytes(a.M, a.N, a.K) || a.ldy != a.N || a.N % 8)
+    return false;
+  GemmArgs b = a;
+  b.splits = sp.splits;
+  b.k_chunk = sp.k_chunk;
+  b.split_stride = static_cast<size_t>(a.M) * a.N;
+  b.Wf = static_cast<float *>(ws);
+  b.db = nullptr;
+  b.accumulate = 0;
+  if (!launch_lds<false, BT, Epi::kF32>(b, s, sp.tile)) return false;
+  const long n8 = static_cast<long>(a.M) * a.N / 8;
+  const int blocks = static_cast<int>(std::min<long>((n8 + 255) / 256, 2048));
+  hipLaunchKernelGGL((splitk_epilogue_kernel<EPI>), dim3(blocks), dim3(256), 0, s, b.Wf, sp.splits, b.split_stride,
+                     a.M, a.N, a.bias, a.R, a.Y, a.Y2);
+  return true;
+}
+
+template <Epi EPI>
+bool fwd_any(const GemmArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
+  return launch_split<false, EPI>(a, ws, ws_bytes, s) || launch_lds<false, false, EPI>(a, s) ||
+         launch_any<false, false, EPI>(a, s);
+}
+
+template <Epi EPI>
+bool dgrad_any(const GemmArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
+  return launch_split<true, EPI>(a, ws, ws_bytes, s) || launch_lds<false, true, EPI>(a, s) ||
+         launch_any<false, true, EPI>(a, s);
+}
+
+}  // namespace
+
+bool launch_gemm_fwd(const GemmArgs &a, Epi epi, void *ws, size_t ws_bytes, hipStream_t s) {
   switch (epi) {
-    case Epi::kBias:
-      return launch_lds<false, false, Epi::kBias>(a, s) || launch_any<false, false, Epi::kBias>(a, s);
-    case Epi::kBiasResid:
-      return launch_lds<false, false, Epi::kBiasResid>(a, s) || launch_any<false, false, Epi::kBiasResid>(a, s);
-    case Epi::kBiasGelu:
-      return launch_lds<false, false, Epi::kBiasGelu>(a, s) || launch_any<false, false, Epi::kBiasGelu>(a, s);
-    case Epi::kPlain:
-      return launch_lds<false, false, Epi::kPlain>(a, s) || launch_any<false, false, Epi::kPlain>(a, s);
+    case Epi::kBias: return fwd_any<Epi::kBias>(a, ws, ws_bytes, s);
+    case Epi::kBiasResid: return fwd_any<Epi::kBiasResid>(a, ws, ws_bytes, s);
+    case Epi::kBiasGelu: return fwd_any<Epi::kBiasGelu>(a, ws, ws_bytes, s);
+    case Epi::kPlain: return fwd_any<Epi::kPlain>(a, ws, ws_bytes, s);
     default: return false;
   }
 }
 
-bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s) {
+bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, void *ws, size_t ws_bytes, hipStream_t s) {
   switch (epi) {
-    case Epi::kPlain:
-      return launch_lds<false, true, Epi::kPlain>(a, s) || launch_any<false, true, Epi::kPlain>(a, s);
-    case Epi::kGeluGrad:
-      return launch_lds<false, true, Epi::kGeluGrad>(a, s) || launch_any<false, true, Epi::kGeluGrad>(a, s);
-    case Epi::kResid:
-      return launch_lds<false, true, Epi::kResid>(a, s) || launch_any<false, true, Epi::kResid>(a, s);
+    case Epi::kPlain: return dgrad_any<Epi::kPlain>(a, ws, ws_bytes, s);
+    case Epi::kGeluGrad: return dgrad_any<Epi::kGeluGrad>(a, ws, ws_bytes, s);
+    case Epi::kResid: return dgrad_any<Epi::kResid>(a, ws, ws_bytes, s);
     default: return false;
   }
 }

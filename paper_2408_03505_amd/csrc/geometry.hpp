@@ -110,7 +110,37 @@ inline SplitPlan wgrad_split_plan(int M, int N, int K) {
   return {1, K, choose_tile(M, N)};
 }
 
+// ---- Forward / input-gradient split plan (output [M, N], contraction K over
+// k-contiguous rows, so K a multiple of 64): a product with at most 32
+// output tiles of 256 x 256 (an eighth of the 256 CUs) and a long
+// contraction is split like a weight gradient; a second kernel adds the fp32
+// partials in split order and applies the epilogue.  The partials' round
+// trip and the separate epilogue pay off only for such very small grids:
+// the ViT-22B shard's out-projection input gradient (24 tiles, K = 6144)
+// took 66 -> 42 us, but with up to 128 tiles the ViT-Base and ViT-Huge
+// forward and input-gradient products with 75-96 tiles ran 5-14 us slower
+// split (the shard's QKV forward, 72 tiles, gained 5 us).
+inline SplitPlan gemm_split_plan(int M, int N, int K) {
+  const long tiles = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
+  if (K % 64 == 0 && tiles * 8 <= 256) {
+    int S = static_cast<int>(std::min<long>(256 / tiles, std::min(K / kMinSplitTokens, kMaxSplits)));
+    if (S > 1) {
+      const int kc = ((K + S - 1) / S + 63) / 64 * 64;
+      S = (K + kc - 1) / kc;
+      if (S > 1) return {S, kc, {256, 256}};
+    }
+  }
+  return {1, K, choose_tile(M, N)};
+}
+
 inline size_t ws_round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// Workspace of a split forward or input-gradient product: the fp32 partials
+// [S][M][N]; 0 when the plan does not split.
+inline size_t gemm_ws_bytes(int M, int N, int K) {
+  const SplitPlan sp = gemm_split_plan(M, N, K);
+  return sp.splits > 1 ? ws_round256(static_cast<size_t>(sp.splits) * M * N * sizeof(float)) : 0;
+}
 
 // Workspace of a split weight gradient: the fp32 partials of dW [S][M][N]
 // and of db [S][M], each 256-byte aligned; 0 when the plan does not split.

@@ -17,8 +17,8 @@ bool launch_ln_bwd(int, int, const bf16_t *, const bf16_t *, const float *, cons
                    const bf16_t *, bf16_t *, float *, float *, int, float *, hipStream_t) {
   return true;
 }
-bool launch_gemm_fwd(const GemmArgs &, Epi, hipStream_t) { return true; }
-bool launch_gemm_dgrad(const GemmArgs &, Epi, hipStream_t) { return true; }
+bool launch_gemm_fwd(const GemmArgs &, Epi, void *, size_t, hipStream_t) { return true; }
+bool launch_gemm_dgrad(const GemmArgs &, Epi, void *, size_t, hipStream_t) { return true; }
 bool launch_gemm_wgrad(const GemmArgs &, void *, size_t, hipStream_t) { return true; }
 bool launch_qk_norm_fwd(int, int, int, const bf16_t *, const bf16_t *, const bf16_t *, const bf16_t *,
                         const bf16_t *, float, bf16_t *, float *, hipStream_t) {

@@ -55,9 +55,12 @@ struct GemmArgs {
 };
 
 // Forward projections: A = X [M, K] row-major, B = W [N, K] row-major.
-bool launch_gemm_fwd(const GemmArgs &a, Epi epi, hipStream_t s);
 // Input gradient: A = dY [M, K] row-major, B(n, k) = W[k, n] (W stored [K, N]).
-bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, hipStream_t s);
+// With a workspace of at least gemm_ws_bytes(M, N, K) bytes, a product whose
+// output tiles leave most CUs idle splits its contraction (gemm_split_plan);
+// ws = nullptr never splits.
+bool launch_gemm_fwd(const GemmArgs &a, Epi epi, void *ws, size_t ws_bytes, hipStream_t s);
+bool launch_gemm_dgrad(const GemmArgs &a, Epi epi, void *ws, size_t ws_bytes, hipStream_t s);
 // Weight gradient: A(m, k) = dY[k, m], B(n, k) = X[k, n] (contraction over tokens).
 // With a workspace of at least gemm_wgrad_ws_bytes(M, N, K) bytes, a problem
 // whose output tiles leave most CUs idle splits the token contraction over

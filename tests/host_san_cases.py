@@ -64,16 +64,16 @@ def test_per_kernel_entry_points_run():
     M, H, A, F = 394, 192, 192, 768
     f = ctypes.c_float(1e-6)
     _ok("enc_ln_fwd", M, H, P, P, P, f, P, P, P, S0)
-    _ok("enc_qkv_fwd", M, H, A, P, P, P, P, S0)
-    _ok("enc_qkv_fwd", M, H, A, P, P, S0, P, S0)  # no bias
+    _ok("enc_qkv_fwd", M, H, A, P, P, P, P, S0, 0, S0)
+    _ok("enc_qkv_fwd", M, H, A, P, P, S0, P, S0, 0, S0)  # no bias
     _ok("enc_attn_fwd", 2, 197, 3, 64, P, P, P, S0)
-    _ok("enc_oproj_fwd", M, A, H, P, P, P, P, P, S0)
-    _ok("enc_mlp_up_fwd", M, H, F, P, P, P, P, P, S0)
-    _ok("enc_mlp_down_fwd", M, F, H, P, P, P, P, P, S0)
-    _ok("enc_mlp_down_bwd_data", M, F, H, P, P, P, P, S0)
-    _ok("enc_mlp_up_bwd_data", M, H, F, P, P, P, S0)
-    _ok("enc_oproj_bwd_data", M, A, H, P, P, P, S0)
-    _ok("enc_qkv_bwd_data", M, H, A, P, P, P, S0)
+    _ok("enc_oproj_fwd", M, A, H, P, P, P, P, P, S0, 0, S0)
+    _ok("enc_mlp_up_fwd", M, H, F, P, P, P, P, P, S0, 0, S0)
+    _ok("enc_mlp_down_fwd", M, F, H, P, P, P, P, P, S0, 0, S0)
+    _ok("enc_mlp_down_bwd_data", M, F, H, P, P, P, P, S0, 0, S0)
+    _ok("enc_mlp_up_bwd_data", M, H, F, P, P, P, S0, 0, S0)
+    _ok("enc_oproj_bwd_data", M, A, H, P, P, P, S0, 0, S0)
+    _ok("enc_qkv_bwd_data", M, H, A, P, P, P, S0, 0, S0)
     _ok("enc_linear_bwd_weight", M, F, H, P, P, P, P, 1, S0, 0, S0)
     _ok("enc_linear_bwd_weight", M, F, H, P, P, P, S0, 0, S0, 0, S0)  # no bias gradient
     # a split weight gradient (small output, many tokens) with its workspace
@@ -88,7 +88,14 @@ def test_per_kernel_entry_points_run():
     _ok("enc_qk_norm_fwd", M, 3, 64, P, P, P, P, P, f, P, P, S0)
     _ok("enc_qk_norm_bwd", M, 3, 64, P, P, P, P, P, P, P, P, P, P, 0, P, B.qk_norm_bwd_workspace_bytes(M, 3, 64),
         S0)
-    _ok("enc_qkv_bwd_data_add", M, H, A, P, P, P, P, S0)
+    _ok("enc_qkv_bwd_data_add", M, H, A, P, P, P, P, S0, 0, S0)
+    # split forward and input-gradient products with their workspaces
+    need = B.linear_workspace_bytes(2048, 1024, 6144)
+    assert need > 0
+    _ok("enc_mlp_up_fwd", 2048, 6144, 1024, P, P, P, P, P, P, need, S0)
+    _ok("enc_mlp_down_bwd_data", 2048, 1024, 6144, P, P, P, P, P, need, S0)
+    need = B.linear_workspace_bytes(2048, 768, 6144)
+    _ok("enc_oproj_bwd_data", 2048, 768, 6144, P, P, P, P, need, S0)
     for cls in (0, 1):
         ws = B.patch_embed_workspace_bytes(2, 3, 224, 224, 14, 192, bool(cls))
         _ok("enc_patch_embed_fwd", 2, 3, 224, 224, 14, 192, cls, P, P, P, P if cls else S0, P, P, P,

@@ -109,8 +109,11 @@ def test_ln_bwd(rows, cols, with_resid):
 # both workgroup orders: one contiguous range per XCD (e.g. 16x18 tiles) and
 # XCDs in two halves along M, including a short last group of row tiles
 # (1536x1536: 12x12 tiles, 6 row tiles per half in groups of 4).
+# The last three split their contraction (at most 32 output tiles of 256 x 256,
+# K >= 1024), one with a ragged M.
 FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
-              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536), (2048, 64, 24576)]
+              (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536), (2048, 64, 24576),
+              (2048, 6144, 1024), (2048, 6144, 768), (1000, 2048, 512)]
 
 
 def _sparse(shape, seed, density):
@@ -177,8 +180,10 @@ def test_mlp_up_fwd(M, K, N):
 
 
 # dgrad: dX[M, K] = dY[M, N] W[N, K]
+# The last three split their contraction (the ViT-22B shard's out-projection
+# input gradient, a 32-tile output, a ragged M).
 BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8),
-                   (2048, 96, 6144), (2048, 128, 6144)]
+                   (2048, 96, 6144), (2048, 128, 6144), (2048, 6144, 768), (2048, 6144, 1024), (1000, 2048, 512)]
 
 
 @pytest.mark.parametrize("M,N,K", BWD_DATA_SHAPES)
@@ -204,6 +209,49 @@ def test_bwd_data_exact(M, N, K):
     if N % 3 == 0 and (N // 3) % 8 == 0:
         ok, err = exact_equal(B.enc_qkv_bwd_data(cuda(dY), cuda(W)), want)
         assert ok, err
+
+
+SPLIT_PRODUCTS = [("qkv_fwd", 2048, 6144, 768), ("mlp_up_fwd", 2048, 6144, 1024), ("oproj_fwd", 1000, 2048, 512),
+                  ("mlp_down_bwd_data", 2048, 6144, 1024), ("oproj_bwd_data", 2048, 6144, 768),
+                  ("qkv_bwd_data", 2048, 2304, 1024)]
+
+
+@pytest.mark.parametrize("kind,M,Kc,N", SPLIT_PRODUCTS)
+def test_split_product_matches_unsplit(kind, M, Kc, N):
+    # Output [M, N], contraction Kc.  The split path (workspace given) and the
+    # unsplit kernel compute the same product and epilogue: both within bf16
+    # rounding of float64, the split path bitwise repeatable.
+    announce(f"split vs unsplit {kind} M={M} K={Kc} N={N}")
+    assert B.linear_workspace_bytes(M, N, Kc) > 0
+    X = cuda(random_bf16((M, Kc), 121))
+    if kind.endswith("_fwd"):
+        W = cuda(random_bf16((N, Kc), 122, 0.05))
+        b = cuda(random_bf16((N,), 123, 0.1))
+        R = cuda(random_bf16((M, N), 124))
+        fn = {"qkv_fwd": lambda split: B.enc_qkv_fwd(X, W, b, split=split),
+              "mlp_up_fwd": lambda split: B.enc_mlp_up_fwd(X, W, b, split=split),
+              "oproj_fwd": lambda split: B.enc_oproj_fwd(X, W, b, R, split=split)}[kind]
+        ref = oracle.linear_fwd(f64(X), f64(W), f64(b), resid=f64(R) if kind == "oproj_fwd" else None)
+    else:
+        W = cuda(random_bf16((Kc, N), 122, 0.05))
+        U = cuda(random_bf16((M, N), 125, 1.5))
+        fn = {"mlp_down_bwd_data": lambda split: B.enc_mlp_down_bwd_data(X, W, U, split=split),
+              "oproj_bwd_data": lambda split: B.enc_oproj_bwd_data(X, W, split=split),
+              "qkv_bwd_data": lambda split: B.enc_qkv_bwd_data(X, W, split=split)}[kind]
+        ref = oracle.linear_bwd_data(f64(X), f64(W))
+        if kind == "mlp_down_bwd_data":
+            ref = ref * oracle.gelu_grad(f64(U))
+    a, a2, u0 = fn(True), fn(True), fn(False)
+    torch.cuda.synchronize()
+    if kind == "mlp_up_fwd":  # (u, g): check u against the product, g against GELU(u)
+        assert torch.equal(a[0], a2[0]) and torch.equal(a[1], a2[1])
+        for got in (a, u0):
+            assert max_rel(f64(got[0]), ref) < 1e-2
+            assert max_rel(f64(got[1]), oracle.gelu(ref)) < 1e-2
+    else:
+        assert torch.equal(a, a2)
+        for got in (a, u0):
+            assert max_rel(f64(got), ref) < 1e-2
 
 
 def _bf16_ulp(v):

@@ -181,12 +181,19 @@ def test_null_and_misaligned_pointers_are_rejected():
     assert _status("enc_ln_fwd", 4, 64, ctypes.c_void_p(FAKE + 2), p, p, ctypes.c_float(1e-6), p, p, p, s) \
         == B.ENC_ERR_ALIGN
     assert b"not 16-byte aligned" in B.lib().enc_last_error()
-    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, p, z, s) == B.ENC_ERR_INVALID  # b_qkv may be NULL, qkv not
-    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, ctypes.c_void_p(FAKE + 4), p, s) == B.ENC_ERR_ALIGN
+    # b_qkv may be NULL, qkv not
+    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, p, z, z, 0, s) == B.ENC_ERR_INVALID
+    assert _status("enc_qkv_fwd", 8, 64, 64, p, p, ctypes.c_void_p(FAKE + 4), p, z, 0, s) == B.ENC_ERR_ALIGN
+    # a product workspace is optional; a given one must be aligned and large enough
+    need = B.linear_workspace_bytes(2048, 1024, 6144)
+    assert need > 0
+    assert _status("enc_mlp_up_fwd", 2048, 6144, 1024, p, p, p, p, p, ctypes.c_void_p(FAKE + 8), need, s) \
+        == B.ENC_ERR_ALIGN
+    assert _status("enc_mlp_up_fwd", 2048, 6144, 1024, p, p, p, p, p, p, need - 1, s) == B.ENC_ERR_WORKSPACE
     assert _status("enc_qk_norm_fwd", 4, 2, 64, p, p, p, z, p, ctypes.c_float(1e-6), p, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_qk_norm_fwd", 4, 2, 96, p, p, p, p, p, ctypes.c_float(1e-6), p, p, s) \
         == B.ENC_ERR_UNSUPPORTED
-    assert _status("enc_qkv_bwd_data_add", 8, 64, 64, p, p, z, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_qkv_bwd_data_add", 8, 64, 64, p, p, z, p, ctypes.c_void_p(0), 0, s) == B.ENC_ERR_INVALID
     assert _status("enc_attn_fwd", 1, 8, 1, 64, p, z, p, s) == B.ENC_ERR_INVALID
     assert _status("enc_linear_bwd_weight", 8, 64, 64, p, p, z, z, 0, z, 0, s) == B.ENC_ERR_INVALID
     # db may be NULL, but a misaligned db is an error
@@ -211,9 +218,9 @@ def test_bad_shapes_are_rejected():
     assert _status("enc_attn_fwd", 1, 116500, 48, 128, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
     assert b"4 GiB" in B.lib().enc_last_error()
     # per-kernel GEMM operands at 2^31 elements are refused
-    assert _status("enc_mlp_down_fwd", 87382, 24576, 64, p, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
-    assert _status("enc_qkv_fwd", 8, 60, 64, p, p, p, p, s) == B.ENC_ERR_UNSUPPORTED
-    assert _status("enc_mlp_up_fwd", -1, 64, 64, p, p, p, p, p, s) == B.ENC_ERR_INVALID
+    assert _status("enc_mlp_down_fwd", 87382, 24576, 64, p, p, p, p, p, ctypes.c_void_p(0), 0, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_qkv_fwd", 8, 60, 64, p, p, p, p, ctypes.c_void_p(0), 0, s) == B.ENC_ERR_UNSUPPORTED
+    assert _status("enc_mlp_up_fwd", -1, 64, 64, p, p, p, p, p, ctypes.c_void_p(0), 0, s) == B.ENC_ERR_INVALID
 
 
 @no_gpu_only

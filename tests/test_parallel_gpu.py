@@ -156,27 +156,28 @@ def test_parallel_block_is_deterministic_and_accumulates():
 
 def _parallel_chain_by_kernels(cfg, x, p, dout):
     """The parallel block through the per-kernel entry points, in the
-    composite's order; returns every step's output."""
+    composite's order, with every product unsplit as the block's composites
+    run them; returns every step's output."""
     Bn, S, nh, d, eps = cfg["batch"], cfg["seq"], cfg["heads"], cfg["head_dim"], cfg["ln_eps"]
     t = {}
     t["y"], t["mean"], t["rstd"] = B.enc_ln_fwd(x, p["ln_g"], p["ln_b"], eps)
-    t["qkv"] = B.enc_qkv_fwd(t["y"], p["w_qkv"], None)
+    t["qkv"] = B.enc_qkv_fwd(t["y"], p["w_qkv"], None, split=False)
     t["qkvn"], t["qkstats"] = B.enc_qk_norm_fwd(nh, d, t["qkv"], p["qn_g"], p["qn_b"], p["kn_g"], p["kn_b"], eps)
     t["o"], t["lse"] = B.enc_attn_fwd(Bn, S, nh, d, t["qkvn"])
-    t["h"] = B.enc_oproj_fwd(t["o"], p["w_o"], p["b_o"], x)
-    t["u"], t["g"] = B.enc_mlp_up_fwd(t["y"], p["w_1"], p["b_1"])
-    t["out"] = B.enc_mlp_down_fwd(t["g"], p["w_2"], p["b_2"], t["h"])
-    t["du"] = B.enc_mlp_down_bwd_data(dout, p["w_2"], t["u"])
-    t["dw_2"], t["db_2"] = B.enc_linear_bwd_weight(dout, t["g"])
-    t["dy_mlp"] = B.enc_mlp_up_bwd_data(t["du"], p["w_1"])
-    t["dw_1"], t["db_1"] = B.enc_linear_bwd_weight(t["du"], t["y"])
-    t["do"] = B.enc_oproj_bwd_data(dout, p["w_o"])
-    t["dw_o"], t["db_o"] = B.enc_linear_bwd_weight(dout, t["o"])
+    t["h"] = B.enc_oproj_fwd(t["o"], p["w_o"], p["b_o"], x, split=False)
+    t["u"], t["g"] = B.enc_mlp_up_fwd(t["y"], p["w_1"], p["b_1"], split=False)
+    t["out"] = B.enc_mlp_down_fwd(t["g"], p["w_2"], p["b_2"], t["h"], split=False)
+    t["du"] = B.enc_mlp_down_bwd_data(dout, p["w_2"], t["u"], split=False)
+    t["dw_2"], t["db_2"] = B.enc_linear_bwd_weight(dout, t["g"], split=False)
+    t["dy_mlp"] = B.enc_mlp_up_bwd_data(t["du"], p["w_1"], split=False)
+    t["dw_1"], t["db_1"] = B.enc_linear_bwd_weight(t["du"], t["y"], split=False)
+    t["do"] = B.enc_oproj_bwd_data(dout, p["w_o"], split=False)
+    t["dw_o"], t["db_o"] = B.enc_linear_bwd_weight(dout, t["o"], split=False)
     t["dqkvn"] = B.enc_attn_bwd(Bn, S, nh, d, t["qkvn"], t["o"], t["lse"], t["do"])
     t["dqkv"], qg = B.enc_qk_norm_bwd(nh, d, t["dqkvn"], t["qkv"], t["qkstats"], p["qn_g"], p["kn_g"])
     t.update({"d" + n: v for n, v in qg.items()})
-    t["dw_qkv"], _ = B.enc_linear_bwd_weight(t["dqkv"], t["y"], with_db=False)
-    t["dy"] = B.enc_qkv_bwd_data_add(t["dqkv"], p["w_qkv"], t["dy_mlp"])
+    t["dw_qkv"], _ = B.enc_linear_bwd_weight(t["dqkv"], t["y"], with_db=False, split=False)
+    t["dy"] = B.enc_qkv_bwd_data_add(t["dqkv"], p["w_qkv"], t["dy_mlp"], split=False)
     t["dx"], t["dln_g"], t["dln_b"] = B.enc_ln_bwd(t["dy"], x, t["mean"], t["rstd"], p["ln_g"], dresid=dout)
     torch.cuda.synchronize()
     return t
