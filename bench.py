@@ -72,8 +72,10 @@ def parse():
 
 
 # GPU kernels of each chain entry, in launch order (a substring of each
-# dispatch's kernel name; every library kernel lives in namespace optimus)
+# dispatch's kernel name; every library kernel lives in namespace optimus).
+# A product whose contraction is split adds its reduction kernel.
 _GEMM = ("gemm_",)
+_GEMM_SPLIT = ("gemm_", "splitk_")
 _LN_BWD = ("ln_bwd_kernel", "ln_bwd_reduce_kernel")
 ENTRY_KERNELS = {"ln1_fwd": ("ln_fwd_kernel",), "qkv_fwd": _GEMM, "attn_fwd": ("attn_fwd_kernel",),
                  "oproj_fwd": _GEMM, "ln2_fwd": ("ln_fwd_kernel",), "mlp_up_fwd": _GEMM, "mlp_down_fwd": _GEMM,
@@ -82,6 +84,35 @@ ENTRY_KERNELS = {"ln1_fwd": ("ln_fwd_kernel",), "qkv_fwd": _GEMM, "attn_fwd": ("
                  "oproj_bwd_weight": _GEMM, "attn_bwd": ("attn_bwd_dq_kernel", "attn_bwd_dkdv_kernel"),
                  "qkv_bwd_data": _GEMM, "qkv_bwd_weight": _GEMM, "ln1_bwd": _LN_BWD}
 DISPATCHES = {n: len(k) for n, k in ENTRY_KERNELS.items()}
+
+
+def gemm_products(cfg):
+    """Each GEMM entry's product as its workspace query takes it: ("fwd", M,
+    N, K) for a forward or input-gradient product with output [M, N] and
+    contraction K; ("wgrad", M, N, K) for the gradient dW[N, K] of a linear
+    layer over M tokens."""
+    Bn, S, H, nh, d, F = (cfg[k] for k in ("batch", "seq", "hidden", "heads", "head_dim", "mlp"))
+    M, A = Bn * S, nh * d
+    return {"qkv_fwd": ("fwd", M, 3 * A, H), "oproj_fwd": ("fwd", M, H, A), "mlp_up_fwd": ("fwd", M, F, H),
+            "mlp_down_fwd": ("fwd", M, H, F), "mlp_down_bwd_data": ("fwd", M, F, H),
+            "mlp_down_bwd_weight": ("wgrad", M, H, F), "mlp_up_bwd_data": ("fwd", M, H, F),
+            "mlp_up_bwd_weight": ("wgrad", M, F, H), "oproj_bwd_data": ("fwd", M, A, H),
+            "oproj_bwd_weight": ("wgrad", M, H, A), "qkv_bwd_data": ("fwd", M, H, 3 * A),
+            "qkv_bwd_weight": ("wgrad", M, 3 * A, H)}
+
+
+def use_config(cfg):
+    """Set the dispatch map for the chain of workload cfg: a product the
+    library splits (it asks for a workspace, which the chain provides) runs
+    as two dispatches."""
+    from paper_2408_03505_amd import binding as B
+    global ENTRY_KERNELS, DISPATCHES
+    ek = dict(ENTRY_KERNELS)
+    for n, (kind, m, nn, k) in gemm_products(cfg).items():
+        need = B.linear_workspace_bytes(m, nn, k) if kind == "fwd" else B.linear_bwd_weight_workspace_bytes(m, nn, k)
+        ek[n] = _GEMM_SPLIT if need > 0 else _GEMM
+    ENTRY_KERNELS = ek
+    DISPATCHES = {n: len(k) for n, k in ek.items()}
 
 
 def is_lib_kernel(name):
@@ -892,6 +923,8 @@ def cpu_baseline(cfg, x, params, dout, budget_s, name=None, seed=0, configs=None
 
 def main():
     args = parse()
+    from paper_2408_03505_amd.synthetic import CONFIGS
+    use_config(CONFIGS[args.config])
     if args.summarize:
         summarize(args.summarize, skip_steps=args.warmup)
         return

@@ -50,6 +50,24 @@ def test_map_dispatches_rejects_partial_steps_and_wrong_kernels():
         bench.map_dispatches(swapped)
 
 
+def test_use_config_counts_the_split_reduction_kernels(monkeypatch):
+    """Products that the library splits at a workload run as two dispatches
+    (the GEMM, then the split reduction); the dispatch map follows."""
+    from paper_2408_03505_amd.synthetic import CONFIGS
+    monkeypatch.setattr(bench, "ENTRY_KERNELS", dict(bench.ENTRY_KERNELS))
+    monkeypatch.setattr(bench, "DISPATCHES", dict(bench.DISPATCHES))
+    gemms = set(bench.gemm_products(CONFIGS["vit22b"]))
+    split_at = {"vit22b": set(), "vit22b_tp8": {"oproj_bwd_data"},
+                "vit_base": {"mlp_down_bwd_weight", "mlp_up_bwd_weight", "oproj_bwd_weight", "qkv_bwd_weight"}}
+    for name, split in split_at.items():
+        bench.use_config(CONFIGS[name])
+        for n in gemms:
+            assert bench.ENTRY_KERNELS[n] == (("gemm_", "splitk_") if n in split else ("gemm_",)), (name, n)
+        names = _one_step_names()
+        steps = bench.map_dispatches([(i, names[i], 1.0) for i in range(len(names))])
+        assert all(steps[0][n] == (2.0 if n in split else 1.0) for n in gemms), name
+
+
 def _write_counters(d, counter, rows):
     os.makedirs(d, exist_ok=True)
     with open(os.path.join(d, "1_counter_collection.csv"), "w", newline="") as fh:

@@ -389,8 +389,10 @@ def test_linear_bwd_weight_without_db():
 
 # --------------------------------------------------------------------------- attention
 
+# Grids of up to 256 workgroups take the small-grid launch shapes, larger
+# ones (the last three cases: 384 forward / dQ workgroups each) the others.
 ATTN_CASES = [(2, 197, 3, 64), (1, 257, 2, 80), (2, 256, 2, 128), (1, 1, 1, 64), (3, 7, 2, 80), (1, 65, 1, 128),
-              (1, 129, 2, 64), (2, 300, 1, 80)]
+              (1, 129, 2, 64), (2, 300, 1, 80), (16, 197, 12, 64), (8, 257, 16, 80), (4, 256, 48, 128)]
 
 
 def _attn_inputs(Bn, S, nh, d, seed, scale):
