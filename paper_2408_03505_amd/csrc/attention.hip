@@ -42,6 +42,7 @@ namespace {
 
 constexpr int kRows = 128;  // queries per forward workgroup: 4 waves x 32
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazyRescale = 8.0f;  // forward: rescale when a query's maximum grows by more than 2^8
 
 // 2^x on the hardware exponential (v_exp_f32).  Every argument here is a
 // logit minus a running maximum or the log-sum-exp, so x <= 0 up to rounding
@@ -306,31 +307,45 @@ __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int h
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) s[f] = mfma32(tile_rows(Ks, f * 32, kk, lane), qf[kk], s[f]);
     }
-    float mt = m;
+    if (k0 + KT > S) {  // the sequence's last, partial tile: keys past it get no weight
+#pragma unroll
+      for (int f = 0; f < NS; ++f)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3) >= S) s[f][i] = -INFINITY;
+    }
+    // Raw logits are scaled by c > 0, so the scaled maximum is c times the
+    // raw one.  The reference maximum m of a query moves only when its
+    // maximum exceeds m by more than kLazyRescale (log2 units); otherwise the
+    // weights, up to 2^kLazyRescale, stay relative to the old m and the
+    // accumulator needs no rescaling.  O = acc / l and lse = m + log2 l hold
+    // for any such m.
+    float ms = -INFINITY;
 #pragma unroll
     for (int f = 0; f < NS; ++f)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-        const float x = (key < S) ? s[f][i] * c : -INFINITY;
-        s[f][i] = x;
-        mt = fmaxf(mt, x);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
-    const float alpha = exp2_hw(m - mt);
-    m = mt;
+      for (int i = 0; i < 16; ++i) ms = fmaxf(ms, s[f][i]);
+    ms = fmaxf(ms, __shfl_xor(ms, 32, kWave));
+    const float mt = ms * c;
+    const bool grow = mt > m + kLazyRescale;
+    if (__any(grow)) {
+      const float mn = grow ? mt : m;
+      const float alpha = exp2_hw(m - mn);  // 0 on the first tile (m = -inf), 1 where m stays
+      m = mn;
+      l *= alpha;
+#pragma unroll
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] *= alpha;
+    }
     float ls = 0.f;
 #pragma unroll
     for (int f = 0; f < NS; ++f)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float pv = exp2_hw(s[f][i] - mt);
+        const float pv = exp2_hw(__builtin_fmaf(s[f][i], c, -m));
         s[f][i] = pv;
         ls += pv;
       }
-    l = l * alpha + ls;
-#pragma unroll
-    for (int nf = 0; nf < H::NF; ++nf) acc[nf] *= alpha;
+    l += ls;
 #pragma unroll
     for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t pb = pack8(s[st >> 1], st & 1);
@@ -440,14 +455,18 @@ __global__ __launch_bounds__(NW * 64, MINB) void attn_bwd_dq_kernel(int B, int S
         dp[f] = mfma32(tile_rows(Vs, f * 32, kk, lane), df[kk], dp[f]);
       }
     }
-    // register i of fragment f is key k0 + f*32 + 8(i/4) + 4 hf + i%4
 #pragma unroll
     for (int f = 0; f < NS; ++f)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-        sv[f][i] = (key < S) ? exp2_hw(sv[f][i] * c - lse2) * (dp[f][i] - dd) : 0.f;  // dS^T
-      }
+      for (int i = 0; i < 16; ++i) sv[f][i] = exp2_hw(__builtin_fmaf(sv[f][i], c, -lse2)) * (dp[f][i] - dd);  // dS^T
+    if (k0 + KT > S) {  // the sequence's last, partial tile: keys past it get no weight
+      // register i of fragment f is key k0 + f*32 + 8(i/4) + 4 hf + i%4
+#pragma unroll
+      for (int f = 0; f < NS; ++f)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (k0 + f * 32 + (i >> 2) * 8 + hf * 4 + (i & 3) >= S) sv[f][i] = 0.f;
+    }
 #pragma unroll
     for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t sb = pack8(sv[st >> 1], st & 1);
@@ -543,10 +562,15 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
   f32x16_t acc[H::NF];  // dV^T (wave A) or dK^T (wave B)
 #pragma unroll
   for (int i = 0; i < H::NF; ++i) acc[i] = f32x16_t{};
-  float *px = reinterpret_cast<float *>(smem_raw + PX) + grp * (32 * KT);
+  constexpr int NS = KT / 32;  // 32-query fragments per tile
+  // P hand-over slot of this key group: lane l's 16 NS values as 16-byte
+  // chunks, chunk j at position j ^ pswz(l); over any 16 consecutive lanes
+  // the positions hit distinct banks, so ds_write_b128 / ds_read_b128 run
+  // without conflicts
+  f32x4_t *pxl = reinterpret_cast<f32x4_t *>(smem_raw + PX) + grp * (8 * KT) + lane * (4 * NS);
+  const int pswz = (lane >> (NS == 1 ? 2 : 1)) & (4 * NS - 1);
   const float c = kLog2e / sqrtf(static_cast<float>(D));
   constexpr int LOADS = 2 * NL;
-  constexpr int NS = KT / 32;  // 32-query fragments per tile
   const int nq = (S + KT - 1) / KT;
   issue(0);
   for (int t = 0; t < nq; ++t) {
@@ -577,6 +601,9 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
       for (int kk = 0; kk < H::KS; ++kk) sv[f] = mfma32(tile_rows(Rs, f * 32, kk, lane), rf[kk], sv[f]);
     }
     if (role_a) {
+      // lse and D of queries past the sequence are not this sequence's: the
+      // last, partial tile zeroes their weights by selection
+      const bool ragged = q0 + KT > S;
 #pragma unroll
       for (int f = 0; f < NS; ++f)
 #pragma unroll
@@ -585,26 +612,30 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
           const f32x4_t l4 = *reinterpret_cast<const f32x4_t *>(Ls + qi) * kLog2e;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float pv = exp2_hw(sv[f][4 * g + e] * c - l4[e]);
-            sv[f][4 * g + e] = q0 + qi + e < S ? pv : 0.f;
-            px[(f * 16 + 4 * g + e) * 64 + lane] = sv[f][4 * g + e];
+            float pv = exp2_hw(__builtin_fmaf(sv[f][4 * g + e], c, -l4[e]));
+            if (ragged && q0 + qi + e >= S) pv = 0.f;
+            sv[f][4 * g + e] = pv;
           }
+          pxl[(f * 4 + g) ^ pswz] = f32x4_t{sv[f][4 * g], sv[f][4 * g + 1], sv[f][4 * g + 2], sv[f][4 * g + 3]};
         }
     }
     }
     lds_barrier();  // P of every group is in LDS
     if (active) {
     if (!role_a) {
+      const bool ragged = q0 + KT > S;
 #pragma unroll
       for (int f = 0; f < NS; ++f)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int qi = f * 32 + 8 * g + 4 * hf;
           const f32x4_t d4 = *reinterpret_cast<const f32x4_t *>(Ls + 64 + qi);
+          const f32x4_t p4 = pxl[(f * 4 + g) ^ pswz];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float pv = px[(f * 16 + 4 * g + e) * 64 + lane];
-            sv[f][4 * g + e] = q0 + qi + e < S ? pv * (sv[f][4 * g + e] - d4[e]) : 0.f;  // dS^T
+            float ds = p4[e] * (sv[f][4 * g + e] - d4[e]);  // dS^T
+            if (ragged && q0 + qi + e >= S) ds = 0.f;
+            sv[f][4 * g + e] = ds;
           }
         }
     }
