@@ -291,10 +291,12 @@ __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int h
   const int nk = (S + KT - 1) / KT;
   for (int t = 0; t < ST - 1 && t < nk; ++t) issue(t);
   for (int t = 0; t < nk; ++t) {
-    if (t + ST - 1 < nk) issue(t + ST - 1);
-    // this wave's loads of the later tiles already issued may stay in flight
-    wait_tiles<2 * NL>(min(nk - 1 - t, ST - 1));
+    // this wave's loads of tile t have landed (those of later tiles may stay in flight)
+    wait_tiles<2 * NL>(min(nk - 1 - t, ST - 2));
+    // every wave's loads of tile t have landed, and every wave is done with
+    // tile t - 1, whose buffer the next issue refills
     block_barrier();
+    if (t + ST - 1 < nk) issue(t + ST - 1);
     const lds_char *Ks = smem + (t % ST) * 2 * TB;
     const lds_char *Vs = Ks + TB;
     const int k0 = t * KT;
@@ -353,12 +355,11 @@ __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int h
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Vs, nf * 32, st, lane), pb, acc[nf]);
     }
     }
-    block_barrier();  // every wave is done with this buffer before it is refilled
   }
+  block_barrier();  // every wave is done with the tile buffers, which the output slots reuse
 
   const float lt = l + __shfl_xor(l, 32, kWave);
   if (qvalid && hf == 0) lse[static_cast<size_t>(bh) * S + q] = (m + log2f(lt)) / kLog2e;
-  // the K/V buffers are free after the loop's last barrier
   const int q0 = qt * kRows + wid * 32;
   store_dmajor_lds<D>(o + (static_cast<size_t>(b) * S + q0) * A + h * D, A, acc, 1.0f / lt, lane,
                       const_cast<lds_char *>(smem) + wid * 8192, S - q0);
@@ -438,9 +439,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void attn_bwd_dq_kernel(int B, int S
   const int nk = (S + KT - 1) / KT;
   for (int t = 0; t < ST - 1 && t < nk; ++t) issue(t);
   for (int t = 0; t < nk; ++t) {
+    wait_tiles<LOADS>(min(nk - 1 - t, ST - 2));  // this wave's loads of tile t
+    block_barrier();  // everyone's loads of tile t landed; tile t - 1's buffer is free
     if (t + ST - 1 < nk) issue(t + ST - 1);
-    wait_tiles<LOADS>(min(nk - 1 - t, ST - 1));
-    block_barrier();
     const lds_char *Ks = smem + (t % ST) * STAGE, *Vs = Ks + TB;
     const int k0 = t * KT;
     if (active) {  // waves whose queries all lie past the sequence only load and synchronise
@@ -474,8 +475,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void attn_bwd_dq_kernel(int B, int S
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Ks, nf * 32, st, lane), sb, acc[nf]);
     }
     }
-    block_barrier();
   }
+  block_barrier();  // the output slots reuse the tile buffers
   const int q0 = qt * ROWS + wid * 32;
   store_dmajor_lds<D>(dqkv + (static_cast<size_t>(b) * S + q0) * ld + h * D, ld, acc,
                       1.0f / sqrtf(static_cast<float>(D)), lane, const_cast<lds_char *>(smem) + wid * 8192, S - q0);
@@ -570,20 +571,14 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
   f32x4_t *pxl = reinterpret_cast<f32x4_t *>(smem_raw + PX) + grp * (8 * KT) + lane * (4 * NS);
   const int pswz = (lane >> (NS == 1 ? 2 : 1)) & (4 * NS - 1);
   const float c = kLog2e / sqrtf(static_cast<float>(D));
-  constexpr int LOADS = 2 * NL;
   const int nq = (S + KT - 1) / KT;
   issue(0);
   for (int t = 0; t < nq; ++t) {
-    if (t + 1 < nq) {
-      issue(t + 1);
-      if (wid < 2)
-        wait_vmcnt<LOADS + 1>();
-      else
-        wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    wait_vmcnt<0>();  // this wave's loads of tile t
+    // every wave's loads of tile t have landed, and every wave is done with
+    // tile t - 1: its buffer is refilled next and its P slots rewritten
     block_barrier();
+    if (t + 1 < nq) issue(t + 1);
     const lds_char *Qs = smem + (t & 1) * STAGE, *Ds = Qs + TB;
     const float *Ls = reinterpret_cast<const float *>(smem_raw + (t & 1) * STAGE + TILES);
     const int q0 = t * KT;
@@ -648,9 +643,9 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
       for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Cs, nf * 32, st, lane), pb, acc[nf]);
     }
     }
-    block_barrier();  // every wave is done with this buffer and the P slots before they are refilled
   }
-  // wave A holds dV, wave B dK; the tile buffers are free after the last barrier
+  block_barrier();  // the output slots reuse the tile buffers
+  // wave A holds dV, wave B dK
   bf16_t *row = dqkv + (static_cast<size_t>(b) * S + k0w) * ld + h * D + (role_a ? 2 * A : A);
   store_dmajor_lds<D>(row, ld, acc, role_a ? 1.0f : 1.0f / sqrtf(static_cast<float>(D)), lane,
                       const_cast<lds_char *>(smem) + wid * 8192, S - k0w);
