@@ -1071,7 +1071,7 @@ bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
 
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s) {
-  return launch_lds<AT, BT, EPI>(a, s, choose_tile(a.M, a.N));
+  return launch_lds<AT, BT, EPI>(a, s, choose_tile(a.M, a.N, AT && BT));
 }
 
 }  // namespace

@@ -57,21 +57,29 @@ inline size_t attn_bwd_ws_bytes(int B, int S, int heads) {
 // one CU (256x256 = 1; 0 = never chosen).  256x128 and 128x256 tiles
 // measured 5-15% slower per GEMM than the shapes below on the ViT-22B
 // tensor-parallel shard, where they would fill more CUs, so they stay off.
-constexpr double kEff256x256 = 1.0, kEff256x192 = 0.95, kEff256x128 = 0.0, kEff128x256 = 0.0, kEff128x128 = 0.75;
+// 128x128 tiles (two workgroups per CU) count 0.9 in the forward and
+// input-gradient layouts: at 0.9 the ViT-Base MLP-up forward and MLP-down
+// input gradient take them and ran 11% faster (58 -> 52 and 61 -> 53 us),
+// while no other product of the five workloads changed tile.  The weight
+// gradients keep 0.75: at 0.9 the ViT-22B shard's MLP weight gradients would
+// take them, and one of the two ran 3% slower.
+constexpr double kEff256x256 = 1.0, kEff256x192 = 0.95, kEff256x128 = 0.0, kEff128x256 = 0.0;
+constexpr double kEff128x128 = 0.9, kEff128x128Wgrad = 0.75;
 
 struct TileShape {
   int bm, bn;
 };
 
-// The tile that minimises (rounds of 256 CUs) x (tile area / efficiency).
-inline TileShape choose_tile(int M, int N) {
+// The tile that minimises (rounds of 256 CUs) x (tile area / efficiency);
+// wgrad selects the weight-gradient layout's efficiencies.
+inline TileShape choose_tile(int M, int N, bool wgrad) {
   auto cost = [&](int bm, int bn, double eff) {
     if (eff <= 0.0) return 1e300;
     const long tiles = static_cast<long>((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return static_cast<double>((tiles + 255) / 256) * bm * bn / eff;
   };
   const TileShape shapes[5] = {{256, 256}, {256, 192}, {256, 128}, {128, 256}, {128, 128}};
-  const double eff[5] = {kEff256x256, kEff256x192, kEff256x128, kEff128x256, kEff128x128};
+  const double eff[5] = {kEff256x256, kEff256x192, kEff256x128, kEff128x256, wgrad ? kEff128x128Wgrad : kEff128x128};
   int best = 0;
   for (int i = 1; i < 5; ++i)
     if (cost(shapes[i].bm, shapes[i].bn, eff[i]) < cost(shapes[best].bm, shapes[best].bn, eff[best])) best = i;
@@ -107,7 +115,7 @@ inline SplitPlan wgrad_split_plan(int M, int N, int K) {
       if (S > 1) return {S, kc, {256, 256}};
     }
   }
-  return {1, K, choose_tile(M, N)};
+  return {1, K, choose_tile(M, N, true)};
 }
 
 // ---- Forward / input-gradient split plan (output [M, N], contraction K over
@@ -130,7 +138,7 @@ inline SplitPlan gemm_split_plan(int M, int N, int K) {
       if (S > 1) return {S, kc, {256, 256}};
     }
   }
-  return {1, K, choose_tile(M, N)};
+  return {1, K, choose_tile(M, N, false)};
 }
 
 inline size_t ws_round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
