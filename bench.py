@@ -144,9 +144,10 @@ def map_dispatches(lib):
 TRAFFIC_MD = os.path.join(ROOT, "profiles", "vit22b_layer_hbm_traffic.md")
 
 
-# Sources each chain entry's kernels are built from (device code and the
-# argument structs they receive): traffic counters describe these files only.
-_COMMON_SRC = ("common.hpp", "lds_dma.hpp", "kernels.hpp")
+# Sources each chain entry's kernels are built from (device code, the
+# argument structs they receive and the launch geometry): traffic counters
+# describe these files only.
+_COMMON_SRC = ("common.hpp", "lds_dma.hpp", "kernels.hpp", "geometry.hpp")
 _FAMILY_SRC = {"gemm": ("gemm.hip",), "attention": ("attention.hip",), "layernorm": ("layernorm.hip",)}
 
 
