@@ -431,6 +431,54 @@ def test_attn_bwd(Bn, S, nh, d):
     assert guard_intact(buf, dqkv.numel())
 
 
+def _climbing_logits_qkv(Bn, S, nh, d, order, seed):
+    """q and k whose logits climb across key tiles: along dimension 0 every
+    query holds +8 (even queries) or -8 (odd queries) and key j holds a ramp
+    r_j, so a query's running maximum grows by up to ~11 log2 units per
+    32-key tile (ascending), only at the first tile (descending), or in
+    uneven steps (zigzag).  Even and odd queries see opposite orders, so
+    within one wave some queries grow while others do not.  The other
+    dimensions hold small noise."""
+    g = torch.Generator().manual_seed(seed)
+    A = nh * d
+    qkv = torch.randn(Bn * S, 3 * A, generator=g) * 0.3
+    j = torch.arange(S, dtype=torch.float32)
+    step = 0.35 / (8.0 * 1.4426950408889634 / d ** 0.5)  # log2 units per key, for |q0| = 8
+    if order == "ascending":
+        r = step * j
+    elif order == "descending":
+        r = step * (S - 1 - j)
+    else:  # zigzag: tiles alternately climb and fall back, the maximum rising in uneven steps
+        t = (j // 32).long()
+        r = step * ((j % 32) * torch.where(t % 2 == 0, 1.0, 0.25) + 9.0 * t)
+    sign = torch.where(torch.arange(S) % 2 == 0, 1.0, -1.0)
+    for h in range(nh):
+        qkv.view(Bn, S, 3 * A)[:, :, h * d] = 8.0 * sign
+        qkv.view(Bn, S, 3 * A)[:, :, A + h * d] = r
+    return qkv.to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("order", ["ascending", "descending", "zigzag"])
+def test_attn_running_maximum_paths(order, d):
+    """The forward rescales a query's accumulator only when its maximum grows
+    by more than 2^8; random inputs rarely reach that after the first tile.
+    Logits that climb across tiles drive the rescale path on every tile,
+    never, or unevenly, with growing and non-growing queries in one wave."""
+    Bn, S, nh = 2, 256, 2
+    announce(f"attention running-maximum paths order={order} d={d}")
+    qkv = _climbing_logits_qkv(Bn, S, nh, d, order, 141)
+    dO = random_bf16((Bn * S, nh * d), 142)
+    o, lse = B.enc_attn_fwd(Bn, S, nh, d, cuda(qkv))
+    dqkv = B.enc_attn_bwd(Bn, S, nh, d, cuda(qkv), o, lse, cuda(dO))
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention_fwd(f64(qkv), Bn, S, nh, d)
+    assert max_rel(f64(o), ro) < TOL_ACT
+    assert np.abs(f64(lse) - rl).max() < 2e-3 * max(1.0, np.abs(rl).max())
+    ref = oracle.attention_bwd(f64(qkv), f64(dO), Bn, S, nh, d)
+    assert max_rel(f64(dqkv), ref) < TOL_GRAD
+
+
 def test_attn_bwd_is_deterministic():
     announce("attn_bwd determinism")
     Bn, S, nh, d = 2, 197, 3, 64
