@@ -43,6 +43,7 @@ namespace {
 constexpr int kRows = 128;  // queries per forward workgroup: 4 waves x 32
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazyRescale = 8.0f;  // forward: rescale when a query's maximum grows by more than 2^8
+constexpr int kPrefetchMaxD = 80;     // head dims whose registers hold a tile's operands read ahead
 
 // 2^x on the hardware exponential (v_exp_f32).  Every argument here is a
 // logit minus a running maximum or the log-sum-exp, so x <= 0 up to rounding
@@ -242,6 +243,29 @@ __device__ __forceinline__ bf16x8_t tile_cols_perm(const lds_char *t, int nbase,
   return lds_read_tr(t + tile_off(k, n >> 3) + in, t + tile_off(k + 8, n >> 3) + in);
 }
 
+// A operands of a token-contracting product (columns nf*32.. of a tile,
+// contraction over its rows), read ahead of the work they wait on when the
+// head is small enough for the registers (PRE); otherwise read at use.
+template <int D, int KT, bool PRE, bool PERM>
+struct ColOperands {
+  bf16x8_t v[PRE ? KT / 16 : 1][PRE ? Head<D>::NF : 1];
+  __device__ __forceinline__ void fetch(const lds_char *t, int lane) {
+    if constexpr (PRE) {
+#pragma unroll
+      for (int st = 0; st < KT / 16; ++st)
+#pragma unroll
+        for (int nf = 0; nf < Head<D>::NF; ++nf)
+          v[st][nf] = PERM ? tile_cols_perm(t, nf * 32, st, lane) : tile_cols(t, nf * 32, st, lane);
+    }
+  }
+  __device__ __forceinline__ bf16x8_t get(const lds_char *t, int nf, int st, int lane) const {
+    if constexpr (PRE)
+      return v[st][nf];
+    else
+      return PERM ? tile_cols_perm(t, nf * 32, st, lane) : tile_cols(t, nf * 32, st, lane);
+  }
+};
+
 template <int D, int KT, int ST, int MINB>
 __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int heads, const bf16_t *__restrict__ qkv,
                                                           uint32_t qkv_bytes, bf16_t *__restrict__ o,
@@ -309,6 +333,8 @@ __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int h
 #pragma unroll
       for (int kk = 0; kk < H::KS; ++kk) s[f] = mfma32(tile_rows(Ks, f * 32, kk, lane), qf[kk], s[f]);
     }
+    ColOperands<D, KT, (D <= kPrefetchMaxD), false> vop;  // V^T operands, read under the softmax
+    vop.fetch(Vs, lane);
     if (k0 + KT > S) {  // the sequence's last, partial tile: keys past it get no weight
 #pragma unroll
       for (int f = 0; f < NS; ++f)
@@ -352,7 +378,7 @@ __global__ __launch_bounds__(256, MINB) void attn_fwd_kernel(int B, int S, int h
     for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t pb = pack8(s[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols(Vs, nf * 32, st, lane), pb, acc[nf]);
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(vop.get(Vs, nf, st, lane), pb, acc[nf]);
     }
     }
   }
@@ -585,6 +611,11 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
     // S^T (wave A) or dP^T (wave B): register 4g+e of fragment f is query
     // f*32 + 8g + 4hf + e (four consecutive queries)
     const lds_char *Rs = role_a ? Qs : Ds;
+    const lds_char *Cs = role_a ? Ds : Qs;
+    // dO^T (wave A) or Q^T (wave B) operands of the token-contracting
+    // product, read while S or dP and the P hand-over run
+    ColOperands<D, KT, (D <= kPrefetchMaxD), true> cop;
+    if (active) cop.fetch(Cs, lane);
     f32x16_t sv[NS];
     // waves whose keys all lie past the sequence only load and synchronise
     // (both waves of a key group agree)
@@ -635,12 +666,11 @@ __global__ __launch_bounds__(NG * 128, MINB) void attn_bwd_dkdv_kernel(int B, in
         }
     }
     // dV^T += dO^T P (wave A) or dK^T += Q^T dS (wave B)
-    const lds_char *Cs = role_a ? Ds : Qs;
 #pragma unroll
     for (int st = 0; st < KT / 16; ++st) {
       const bf16x8_t pb = pack8(sv[st >> 1], st & 1);
 #pragma unroll
-      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(tile_cols_perm(Cs, nf * 32, st, lane), pb, acc[nf]);
+      for (int nf = 0; nf < H::NF; ++nf) acc[nf] = mfma32(cop.get(Cs, nf, st, lane), pb, acc[nf]);
     }
     }
   }
