@@ -125,11 +125,12 @@ __device__ __forceinline__ void store_dmajor_lds(bf16_t *dst, size_t ld, const f
 
 // ------------------------------------------------------------------ forward
 //
-// K and V tiles of 64 tokens go HBM -> LDS by DMA (double-buffered, no
-// staging registers), rows of kDL = 128 columns taken from the head's first
-// column (columns past head_dim belong to the neighbouring data and are
-// never contracted; rows past the sequence belong to the next sequence or
-// read as zero past the tensor, and are masked out of the softmax).  K is
+// K and V tiles of KT tokens (32, or 64 on grids that leave CUs idle) go
+// HBM -> LDS by DMA (double-buffered, no staging registers), rows of
+// kDL = 128 columns taken from the head's first column (columns past
+// head_dim belong to the neighbouring data and are never contracted; rows
+// past the sequence re-read the tile's first row and are masked out of the
+// softmax).  K is
 // read as the A operand of S^T = K Q^T with ds_read_b128; V is read as the A
 // operand of O^T += V^T P^T with ds_read_b64_tr_b16.  The transpose read
 // delivers tokens in natural order while the P^T registers hold them with
