@@ -844,6 +844,15 @@ def step_flops(cfg):
     return sum(f for f, _ in kernel_work(cfg).values())
 
 
+def hardware_flops(cfg):
+    """Flops the kernels execute where they differ from the algorithmic
+    count: the attention backward recomputes S (in both of its kernels) and
+    dP (in both), so it runs seven 2*B*heads*S^2*d products (dQ kernel: S,
+    dP, dQ; dK/dV kernel: S, dP, dV, dK) against the four counted."""
+    Bn, S, nh, d = (cfg[k] for k in ("batch", "seq", "heads", "head_dim"))
+    return {"attn_bwd": 7 * 2 * Bn * nh * S * S * d}
+
+
 def cpu_model():
     """The host CPU's model name (first processor in /proc/cpuinfo)."""
     try:
@@ -1023,6 +1032,8 @@ def main():
                       "gbs": round(work[n][1] / (p50[n] * 1e-6) / 1e9, 1),
                       "frac": round((work[n][0] / (p50[n] * 1e-6) / 1e12) / PEAK_BF16_TFLOPS, 3) if work[n][0]
                       else round(work[n][1] / (p50[n] * 1e-6) / 1e9 / PEAK_HBM_GBS, 3)} for n in names}
+    for n, hw in hardware_flops(cfg).items():
+        per_kernel[n]["hw_tflops"] = round(hw / (p50[n] * 1e-6) / 1e12, 1)
 
     res = {
         "metric": "encoder layer fwd+bwd TFLOPS (% bf16 MFMA peak) + per-kernel p50 latency (us)",

@@ -120,6 +120,8 @@ def test_kernel_work_covers_every_entry():
         assert all(f >= 0 and b > 0 for f, b in work.values())
         # memory-bound entries carry no flops; every other entry does
         assert all((work[n][0] == 0) == (n in bench.MEM_BOUND) for n in work)
+        # the attention backward's kernels run 7 products where 4 are counted
+        assert bench.hardware_flops(cfg)["attn_bwd"] * 4 == work["attn_bwd"][0] * 7
 
 
 def test_bubble_fit_packs_in_chain_order():
