@@ -845,6 +845,162 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
   }
 }
 
+// Variant of the two-stage kernel with uneven operand rings: the deep
+// operand (A when A_DEEP, else B) cycles through three LDS slots and is
+// refilled two stages ahead, the other through two slots, one stage ahead.
+// A 256x192x64 tile uses 3 x 32 + 2 x 24 KB = 144 KB (a 256x256 one would
+// take all 160 KB).  Each stage issues the shallow operand's next stage
+// first and the deep operand's stage a sub-step later (kDeepSpread), so the
+// wait that ends the stage leaves exactly the latter in flight; one barrier
+// per stage as in the two-stage kernel.  A stage's refill then has two
+// stages of matrix work to land in instead of one.
+constexpr bool kDeepSpread = true;
+
+template <int BM, int BN, int BK, int WM, int WN, bool A_DEEP, bool BT, Epi EPI>
+__global__ __launch_bounds__(WM *WN * 64, 1) void gemm_deep_kernel(GemmArgs p, uint32_t a_bytes, uint32_t b_bytes) {
+  constexpr int NW = WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int KS = BK / 16;
+  using LA = DirectLoader<BM, BK, NW, false>;
+  using LB = DirectLoader<BN, BK, NW, BT>;
+  constexpr int A_BYTES = LA::BYTES, B_BYTES = LB::BYTES;
+  constexpr int SA = A_DEEP ? 3 : 2, SB = A_DEEP ? 2 : 3;
+  constexpr int B_BASE = SA * A_BYTES;
+  constexpr int NX = A_DEEP ? LA::NI : LB::NI;  // loads per wave of one stage of the deep operand
+  static_assert(KS % 2 == 0, "fragment double-buffering needs an even number of k-steps per stage");
+  extern __shared__ __attribute__((aligned(1024))) char smem_raw[];
+  const lds_char *smem = (const lds_char *)(smem_raw);
+
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wid / WN, wn = wid % WN;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  int tm, tn, kbeg, klen;
+  const int split = split_of(p, tiles_m, tiles_n, tm, tn, kbeg, klen);
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  LA la;
+  LB lb;
+  la.init(p.A, a_bytes, p.lda, m0, wid, lane);
+  lb.init(p.B, b_bytes, p.ldb, n0, wid, lane);
+  const uint32_t a_k0 = static_cast<uint32_t>(kbeg) * 2;
+  const uint32_t b_step = BT ? static_cast<uint32_t>(BK) * p.ldb * 2 : BK * 2;
+  const uint32_t b_k0 = BT ? static_cast<uint32_t>(kbeg) * p.ldb * 2 : static_cast<uint32_t>(kbeg) * 2;
+  FragAddr<BM, BK, FM, false> fa;
+  FragAddr<BN, BK, FN, BT> fb;
+  fa.init(wm * WTM, lane);
+  fb.init(wn * WTN, lane);
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+
+  const int nk = (klen + BK - 1) / BK;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+  auto issue_a = [&](int t) { la.issue(lds0 + (t % SA) * A_BYTES, a_k0 + t * BK * 2, wid); };
+  auto issue_b = [&](int t) { lb.issue(lds0 + B_BASE + (t % SB) * B_BYTES, b_k0 + t * b_step, wid); };
+  auto issue_deep = [&](int t) {
+    if constexpr (A_DEEP)
+      issue_a(t);
+    else
+      issue_b(t);
+  };
+  auto issue_shallow = [&](int t) {
+    if constexpr (A_DEEP)
+      issue_b(t);
+    else
+      issue_a(t);
+  };
+  auto a_stage = [&](int t) { return smem + (t % SA) * A_BYTES; };
+  auto b_stage = [&](int t) { return smem + B_BASE + (t % SB) * B_BYTES; };
+
+  // stage 0 of both operands, then stage 1 of the deep one
+  issue_deep(0);
+  issue_shallow(0);
+  if (nk > 1) {
+    issue_deep(1);
+    wait_vmcnt<NX>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+
+  bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) af[0][i] = fa.get(a_stage(0), i, 0);
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bfr[0][j] = fb.get(b_stage(0), j, 0);
+
+  for (int t = 0; t < nk; ++t) {
+    // refill the slots stage t-1 used (every wave finished reading them
+    // before the barrier that ended stage t-1): shallow operand first
+    if (t + 1 < nk) issue_shallow(t + 1);
+    if (!kDeepSpread && t + 2 < nk) issue_deep(t + 2);
+    const lds_char *As = a_stage(t), *Bs = b_stage(t);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int c = kk & 1, n = c ^ 1;
+      // the deep operand has two stages of lead: its refill can go out a
+      // sub-step after the shallow one's
+      if (kDeepSpread && kk == 1 && t + 2 < nk) issue_deep(t + 2);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(bfr[c][j], af[c][i], acc[i][j]);
+      if (kk + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[n][i] = fa.get(As, i, kk + 1);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[n][j] = fb.get(Bs, j, kk + 1);
+        interleave_reads<FM * FN, (FM + FN) * (BT ? 2 : 1)>();
+      } else if (t + 1 < nk) {
+        // stage t+1 of both operands landed for this wave (the deep
+        // operand's stage t+2, issued last, may stay in flight); this
+        // wave's LDS reads of stage t retired
+        if (t + 2 < nk)
+          wait_vmcnt<NX, 0>();
+        else
+          wait_vmcnt<0, 0>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[n][i] = fa.get(a_stage(t + 1), i, 0);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[n][j] = fb.get(b_stage(t + 1), j, 0);
+      }
+    }
+  }
+  const GemmArgs q = split_outputs(p, split);
+  store_tile_lds<EPI, BM, BN, WM, WN>(q, acc, m0, n0, wm, wn, lane, reinterpret_cast<float *>(smem_raw));
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool A_DEEP, bool BT, Epi EPI>
+bool launch_deep_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
+  constexpr int NW = WM * WN;
+  constexpr size_t lds = static_cast<size_t>(A_DEEP ? 3 : 2) * DirectLoader<BM, BK, NW, false>::BYTES +
+                         static_cast<size_t>(A_DEEP ? 2 : 3) * DirectLoader<BN, BK, NW, BT>::BYTES;
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (a.splits > 1 ? a.splits : 1);
+  hipLaunchKernelGGL((gemm_deep_kernel<BM, BN, BK, WM, WN, A_DEEP, BT, EPI>), dim3(tiles), dim3(NW * 64), lds, s, a,
+                     a_bytes, b_bytes);
+  return true;
+}
+
+// 256x192 products that take the uneven-ring kernel (A deep): forward-layout
+// products with a contraction longer than kDeepFwdMinK.  Measured (same-box
+// A/B, ViT-22B layer): MLP-down forward (K = 24576) 543 -> 508 us; at
+// K = 6144 (QKV and out-projection forward) 1% slower than the two-stage
+// kernel, whose refill spread applies there; input gradients 0-8% slower
+// (kDeepDgrad), 256x256 forward tiles 1-5% slower.
+constexpr int kDeepFwdMinK = 8192;
+constexpr bool kDeepDgrad = false;
+
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
 bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
   constexpr int NW = WM * WN;
@@ -1040,6 +1196,7 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 //   tile      forward (A, B k-contiguous)  input gradient (B strided)  weight gradient (both strided)
 //   256x256   gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage  gemm_pp_kernel BK32 4-stage
 //   256x192   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage
+//             (K > 8192: gemm_deep_kernel)
 //   128x128   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage
 // The ping-pong schedule hides the transpose reads of strided operands
 // better where it is used; on the 256x192 input gradients it measured no
@@ -1062,6 +1219,9 @@ bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
   }
   if (t.bm == 256 && t.bn == 192) {
     if constexpr (AT && BT) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+    if constexpr (!AT) {
+      if (BT ? kDeepDgrad : a.K > kDeepFwdMinK) return launch_deep_cfg<256, 192, BK, 4, 2, true, BT, EPI>(a, ab, bb, s);
+    }
     return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
   }
   if (t.bm == 256) return launch_lds_cfg<256, 128, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);

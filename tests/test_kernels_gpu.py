@@ -113,7 +113,9 @@ def test_ln_bwd(rows, cols, with_resid):
 # K >= 1024), one with a ragged M.
 FWD_SHAPES = [(394, 192, 576), (300, 200, 1280), (2048, 768, 2304), (2000, 72, 16384), (33, 8, 8),
               (2048, 256, 16384), (1000, 96, 4096), (2048, 128, 6144), (1536, 128, 1536), (2048, 64, 24576),
-              (2048, 6144, 1024), (2048, 6144, 768), (1000, 2048, 512)]
+              (2048, 6144, 1024), (2048, 6144, 768), (1000, 2048, 512),
+              # 256x192 tiles with a contraction past 8192: the uneven-ring kernel, ragged M
+              (2000, 8256, 6144)]
 
 
 def _sparse(shape, seed, density):
