@@ -997,7 +997,8 @@ bool launch_deep_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipS
 // A/B, ViT-22B layer): MLP-down forward (K = 24576) 543 -> 508 us; at
 // K = 6144 (QKV and out-projection forward) 1% slower than the two-stage
 // kernel, whose refill spread applies there; input gradients 0-8% slower
-// (kDeepDgrad), 256x256 forward tiles 1-5% slower.
+// with A deep (kDeepDgrad) and equal to 8% slower with B deep, 256x256
+// forward tiles 1-5% slower.
 constexpr int kDeepFwdMinK = 8192;
 constexpr bool kDeepDgrad = false;
 
