@@ -1002,6 +1002,12 @@ bool launch_deep_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipS
 constexpr int kDeepFwdMinK = 8192;
 constexpr bool kDeepDgrad = false;
 
+// 256x192 input gradients with a contraction longer than this take the
+// ping-pong kernel: same-box A/B on the ViT-22B layer, MLP-up input gradient
+// (K = 24576) 531 -> 523 us and QKV input gradient (K = 18432) 402 -> 396 us;
+// at K = 6144 (out-projection) it was no better.
+constexpr int kPpDgradMinK = 8192;
+
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
 bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
   constexpr int NW = WM * WN;
@@ -1197,11 +1203,11 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 //   tile      forward (A, B k-contiguous)  input gradient (B strided)  weight gradient (both strided)
 //   256x256   gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage  gemm_pp_kernel BK32 4-stage
 //   256x192   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage
-//             (K > 8192: gemm_deep_kernel)
+//             (K > 8192: gemm_deep_kernel)  (K > 8192: gemm_pp_kernel)
 //   128x128   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage
 // The ping-pong schedule hides the transpose reads of strided operands
-// better where it is used; on the 256x192 input gradients it measured no
-// better than the two-stage kernel.
+// better where it is used; on the 256x192 input gradients it helps only with
+// long contractions.
 // Returns false when the operands do not fit the path's constraints.
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
@@ -1220,6 +1226,9 @@ bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
   }
   if (t.bm == 256 && t.bn == 192) {
     if constexpr (AT && BT) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+    if constexpr (!AT && BT) {
+      if (a.K > kPpDgradMinK) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
+    }
     if constexpr (!AT) {
       if (BT ? kDeepDgrad : a.K > kDeepFwdMinK) return launch_deep_cfg<256, 192, BK, 4, 2, true, BT, EPI>(a, ab, bb, s);
     }
