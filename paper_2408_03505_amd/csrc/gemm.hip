@@ -1003,10 +1003,12 @@ constexpr int kDeepFwdMinK = 8192;
 constexpr bool kDeepDgrad = false;
 
 // 256x192 input gradients with a contraction longer than this take the
-// ping-pong kernel: same-box A/B on the ViT-22B layer, MLP-up input gradient
-// (K = 24576) 531 -> 523 us and QKV input gradient (K = 18432) 402 -> 396 us;
-// at K = 6144 (out-projection) it was no better.
-constexpr int kPpDgradMinK = 8192;
+// ping-pong kernel.  Same-box A/B on the ViT-22B layer: alone, the MLP-up
+// input gradient (K = 24576) went 531 -> 523 us and the QKV one
+// (K = 18432) 402 -> 396 us; inside the layer chain the MLP-up one still
+// gained (541 -> 535 us) but the QKV one lost (401 -> 409 us), and at
+// K = 6144 (out-projection) it was no better.
+constexpr int kPpDgradMinK = 20480;
 
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
 bool launch_lds_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStream_t s) {
@@ -1203,7 +1205,7 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 //   tile      forward (A, B k-contiguous)  input gradient (B strided)  weight gradient (both strided)
 //   256x256   gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage  gemm_pp_kernel BK32 4-stage
 //   256x192   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_pp_kernel BK32 4-stage
-//             (K > 8192: gemm_deep_kernel)  (K > 8192: gemm_pp_kernel)
+//             (K > 8192: gemm_deep_kernel)  (K > 20480: gemm_pp_kernel)
 //   128x128   gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage  gemm_lds_kernel BK64 2-stage
 // The ping-pong schedule hides the transpose reads of strided operands
 // better where it is used; on the 256x192 input gradients it helps only with

@@ -186,8 +186,8 @@ def test_mlp_up_fwd(M, K, N):
 # input gradient, a 32-tile output, a ragged M).
 BWD_DATA_SHAPES = [(394, 576, 192), (300, 1280, 200), (2048, 2304, 768), (2000, 256, 16384), (9, 8, 8),
                    (2048, 96, 6144), (2048, 128, 6144), (2048, 6144, 768), (2048, 6144, 1024), (1000, 2048, 512),
-                   # 256x192 tiles with a contraction past 8192: the ping-pong kernel, ragged M
-                   (2000, 8256, 6144)]
+                   # 256x192 tiles with a contraction past 20480: the ping-pong kernel, ragged M
+                   (2000, 20544, 6144)]
 
 
 @pytest.mark.parametrize("M,N,K", BWD_DATA_SHAPES)
