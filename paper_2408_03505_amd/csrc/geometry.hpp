@@ -86,18 +86,19 @@ inline TileShape choose_tile(int M, int N, bool wgrad) {
   return shapes[best];
 }
 
-// ---- Weight-gradient split plan (M output rows, N output columns, K tokens).
-// A weight gradient with at most 64 output tiles of 256 x 256 (a quarter of
-// the 256 CUs) is split over the tokens: enough splits to fill the CUs, each
-// covering at least kMinSplitTokens tokens in a whole number of 64-wide
-// k-steps (the last split takes the remainder).  Split problems keep
-// 256 x 256 tiles: every split re-reads its operand panels, and 128 x 128
-// tiles (half the flops per operand byte) made the splits bandwidth-bound.
-// Measured per layer (ViT-Base / ViT-Huge / ViT-22B shard, four weight
-// gradients): 351 -> 201 us, 287 -> 268 us, 299 -> 299 us; splitting up to
-// 128 tiles lost 10-20 us on the ViT-Huge MLP and shard out-projection
-// gradients, and at most 8 or 4 splits gained less.  Otherwise the tile
-// comes from choose_tile and nothing is split.
+// ---- Split of the contraction.  A product whose output is a small grid of
+// 256 x 256 tiles is split over its contraction (the tokens, for a weight
+// gradient): each split writes fp32 partials and a second kernel adds them
+// in split order (deterministic).  Splits run 128 x 128 tiles, as many splits
+// as fill two workgroups on each of the 256 CUs, each covering at least
+// kMinSplitTokens of the contraction in a whole number of 64-wide k-steps
+// (the last split takes the remainder).  Same-box A/B of the split kernels
+// alone (us): with 256 x 256 tiles split to fill the CUs once, the ViT-Base
+// weight gradients took 60, 58, 35 and 47 (MLP-down, MLP-up, out-projection,
+// QKV); with the 128 x 128 splits 53, 56, 26 and 40, the ViT-Huge
+// out-projection weight gradient 39 -> 30 and the ViT-22B shard's
+// out-projection input gradient 44 -> 36.  In the layer chain ViT-Base went
+// from 0.665 to 0.631 ms per step; ViT-Huge and the shard were unchanged.
 constexpr int kMinSplitTokens = 512, kMaxSplits = 16;
 
 struct SplitPlan {
@@ -105,38 +106,43 @@ struct SplitPlan {
   TileShape tile;
 };
 
+inline SplitPlan split_128(int M, int N, int K) {
+  const long tiles = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+  int S = static_cast<int>(std::min<long>(512 / tiles, std::min(K / kMinSplitTokens, kMaxSplits)));
+  if (S > 1) {
+    const int kc = ((K + S - 1) / S + 63) / 64 * 64;
+    S = (K + kc - 1) / kc;
+    if (S > 1) return {S, kc, {128, 128}};
+  }
+  return {1, K, {0, 0}};
+}
+
+// Weight gradient (M output rows, N output columns, K tokens): split when
+// the output has at most 64 tiles of 256 x 256 (a quarter of the CUs).
+// Measured per layer with the earlier 256 x 256 splits (ViT-Base / ViT-Huge /
+// ViT-22B shard, four weight gradients): 351 -> 201 us, 287 -> 268 us,
+// 299 -> 299 us against no split; splitting outputs of up to 128 tiles lost
+// 10-20 us on the ViT-Huge MLP and shard out-projection gradients.
 inline SplitPlan wgrad_split_plan(int M, int N, int K) {
   const long tiles = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
   if (tiles * 4 <= 256) {
-    int S = static_cast<int>(std::min<long>(256 / tiles, std::min(K / kMinSplitTokens, kMaxSplits)));
-    if (S > 1) {
-      const int kc = ((K + S - 1) / S + 63) / 64 * 64;
-      S = (K + kc - 1) / kc;
-      if (S > 1) return {S, kc, {256, 256}};
-    }
+    const SplitPlan sp = split_128(M, N, K);
+    if (sp.splits > 1) return sp;
   }
   return {1, K, choose_tile(M, N, true)};
 }
 
-// ---- Forward / input-gradient split plan (output [M, N], contraction K over
-// k-contiguous rows, so K a multiple of 64): a product with at most 32
-// output tiles of 256 x 256 (an eighth of the 256 CUs) and a long
-// contraction is split like a weight gradient; a second kernel adds the fp32
-// partials in split order and applies the epilogue.  The partials' round
+// Forward / input-gradient product (output [M, N], contraction K over
+// k-contiguous rows, so K a multiple of 64): split when the output has at
+// most 32 tiles of 256 x 256 (an eighth of the CUs).  The partials' round
 // trip and the separate epilogue pay off only for such very small grids:
-// the ViT-22B shard's out-projection input gradient (24 tiles, K = 6144)
-// took 66 -> 42 us, but with up to 128 tiles the ViT-Base and ViT-Huge
-// forward and input-gradient products with 75-96 tiles ran 5-14 us slower
-// split (the shard's QKV forward, 72 tiles, gained 5 us).
+// with up to 128 tiles the ViT-Base and ViT-Huge forward and input-gradient
+// products with 75-96 tiles ran 5-14 us slower split.
 inline SplitPlan gemm_split_plan(int M, int N, int K) {
   const long tiles = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
   if (K % 64 == 0 && tiles * 8 <= 256) {
-    int S = static_cast<int>(std::min<long>(256 / tiles, std::min(K / kMinSplitTokens, kMaxSplits)));
-    if (S > 1) {
-      const int kc = ((K + S - 1) / S + 63) / 64 * 64;
-      S = (K + kc - 1) / kc;
-      if (S > 1) return {S, kc, {256, 256}};
-    }
+    const SplitPlan sp = split_128(M, N, K);
+    if (sp.splits > 1) return sp;
   }
   return {1, K, choose_tile(M, N, false)};
 }
