@@ -997,10 +997,9 @@ bool launch_deep_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipS
 // A/B, ViT-22B layer): MLP-down forward (K = 24576) 543 -> 508 us; at
 // K = 6144 (QKV and out-projection forward) 1% slower than the two-stage
 // kernel, whose refill spread applies there; input gradients 0-8% slower
-// with A deep (kDeepDgrad) and equal to 8% slower with B deep, 256x256
-// forward tiles 1-5% slower.
+// with A deep and equal to 8% slower with B deep, 256x256 forward tiles
+// 1-5% slower.  So only the forward layout with A deep is instantiated.
 constexpr int kDeepFwdMinK = 8192;
-constexpr bool kDeepDgrad = false;
 
 // 256x192 input gradients with a contraction longer than this take the
 // ping-pong kernel.  Same-box A/B on the ViT-22B layer: alone, the MLP-up
@@ -1231,8 +1230,8 @@ bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
     if constexpr (!AT && BT) {
       if (a.K > kPpDgradMinK) return launch_pp_cfg<256, 192, 32, 4, 2, 4, AT, BT, EPI>(a, ab, bb, s);
     }
-    if constexpr (!AT) {
-      if (BT ? kDeepDgrad : a.K > kDeepFwdMinK) return launch_deep_cfg<256, 192, BK, 4, 2, true, BT, EPI>(a, ab, bb, s);
+    if constexpr (!AT && !BT) {
+      if (a.K > kDeepFwdMinK) return launch_deep_cfg<256, 192, BK, 4, 2, true, false, EPI>(a, ab, bb, s);
     }
     return launch_lds_cfg<256, 192, BK, 4, 2, 2, AT, BT, EPI>(a, ab, bb, s);
   }
