@@ -101,6 +101,76 @@ def gemm_products(cfg):
             "qkv_bwd_weight": ("wgrad", M, 3 * A, H)}
 
 
+def _tile_of(pid, nb, tiles_m, tiles_n):
+    """Output tile of workgroup pid in an unsplit GEMM grid of nb workgroups,
+    in the kernels' order (workgroup i runs on XCD i % 8): with an even grid,
+    two M-halves of four XCDs each, every XCD walking its block in groups of
+    4 row tiles; otherwise one contiguous range of tiles per XCD, in groups
+    of 8 row tiles."""
+    xcd, local = pid & 7, pid >> 3
+    if tiles_m % 2 == 0 and tiles_n % 4 == 0:
+        rows_p, cols_x = tiles_m // 2, tiles_n // 4
+        g, in_g = divmod(local, 4 * cols_x)
+        gm = min(rows_p - 4 * g, 4)
+        return (xcd >> 2) * rows_p + 4 * g + in_g % gm, (xcd & 3) * cols_x + in_g // gm
+    per, rem = nb >> 3, nb & 7
+    logical = xcd * (per + 1) + local if xcd < rem else rem * (per + 1) + (xcd - rem) * per + local
+    g, in_g = divmod(logical, 8 * tiles_n)
+    gm = min(tiles_m - 8 * g, 8)
+    return 8 * g + in_g % gm, in_g // gm
+
+
+def _split_item(pid, nb, tiles_m, tiles_n):
+    """(split, row tile, column tile) of workgroup pid in a split grid: work
+    items split-major and M-fastest, one contiguous range per XCD."""
+    xcd, local = pid & 7, pid >> 3
+    per, rem = nb >> 3, nb & 7
+    item = xcd * (per + 1) + local if xcd < rem else rem * (per + 1) + (xcd - rem) * per + local
+    split, t = divmod(item, tiles_m * tiles_n)
+    return split, t % tiles_m, t // tiles_m
+
+
+def fetch_floor(rows, cols, K, bm, bn, splits):
+    """Operand bytes the eight L2s must fetch at least for one GEMM launch
+    (output rows x cols, contraction K, bf16 operands): the workgroups of a
+    round run together (one per CU, two for 128x128 tiles), the eighth of
+    them on one XCD share its L2, and an operand panel (a tile row's or tile
+    column's slice of the contraction) outlives neither its round nor its
+    XCD.  Each round's distinct panels per XCD, summed."""
+    per_round = 512 if (bm, bn) == (128, 128) else 256
+    tm, tn = -(-rows // bm), -(-cols // bn)
+    nb = tm * tn * splits
+    kc = -(-K // splits) if splits > 1 else K
+    if splits > 1:
+        kc = -(-kc // 64) * 64
+    total = 0
+    for r0 in range(0, nb, per_round):
+        panels = {}
+        for pid in range(r0, min(nb, r0 + per_round)):
+            sp, a, b = _split_item(pid, nb, tm, tn) if splits > 1 else (0, *_tile_of(pid, nb, tm, tn))
+            klen = min(K - sp * kc, kc)
+            rs, cs = panels.setdefault(pid & 7, (set(), set()))
+            rs.add((a, sp, min(bm, rows - a * bm) * klen))
+            cs.add((b, sp, min(bn, cols - b * bn) * klen))
+        total += sum(2 * (sum(x[2] for x in rs) + sum(x[2] for x in cs)) for rs, cs in panels.values())
+    return total
+
+
+def gemm_fetch_floors(cfg):
+    """fetch_floor of every GEMM entry under the library's own launch plan."""
+    from paper_2408_03505_amd import binding as B
+    out = {}
+    for n, (kind, m, nn, k) in gemm_products(cfg).items():
+        if kind == "wgrad":  # dW[nn, k] over m tokens
+            bm, bn, sp = B.linear_plan(B.LAYOUT_WGRAD, m, nn, k)
+            out[n] = fetch_floor(nn, k, m, bm, bn, sp)
+        else:
+            layout = B.LAYOUT_DGRAD if n.endswith("_bwd_data") else B.LAYOUT_FWD
+            bm, bn, sp = B.linear_plan(layout, m, nn, k)
+            out[n] = fetch_floor(m, nn, k, bm, bn, sp)
+    return out
+
+
 def use_config(cfg):
     """Set the dispatch map for the chain of workload cfg: a product the
     library splits (it asks for a workspace, which the chain provides) runs
@@ -957,11 +1027,17 @@ def main():
         for fam in sorted(_FAMILY_SRC):
             print(f"source-sha256 {fam}: {source_hash(fam)}")
         print(f"copy-reference-bytes: {args.copy_mib << 20}  fetch-scale: {fs:.4f}  write-scale: {ws:.4f}\n")
-        print("| entry | FETCH bytes | WRITE bytes | traffic bytes | algorithmic bytes | traffic / algorithmic |")
-        print("|---|---|---|---|---|---|")
+        floors = gemm_fetch_floors(CONFIGS[args.config])
+        print("`fetch floor`: for each GEMM, the operand bytes that the eight XCD caches must fetch at least "
+              "under its launch plan, since each XCD's concurrent workgroups share one L2 and an operand "
+              "panel outlives neither its round of tiles nor its XCD.\n")
+        print("| entry | FETCH bytes | WRITE bytes | traffic bytes | algorithmic bytes | traffic / algorithmic "
+              "| fetch floor | FETCH / floor |")
+        print("|---|---|---|---|---|---|---|---|")
         for n in DISPATCHES:
             t = fetch[n] + write[n]
-            print(f"| {n} | {fetch[n]:.0f} | {write[n]:.0f} | {t:.0f} | {work[n][1]} | {t / work[n][1]:.2f} |")
+            fl = f"{floors[n]} | {fetch[n] / floors[n]:.2f}" if n in floors else " | "
+            print(f"| {n} | {fetch[n]:.0f} | {write[n]:.0f} | {t:.0f} | {work[n][1]} | {t / work[n][1]:.2f} | {fl} |")
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are out of scope "

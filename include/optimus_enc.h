@@ -543,6 +543,21 @@ int enc_calib_mfma(int blocks, int iters, float *out, enc_stream_t stream);
  * overlap. */
 int enc_calib_copy(const void *src, void *dst, size_t bytes, enc_stream_t stream);
 
+/* Launch plan of one projection product, for tools that model its memory
+ * traffic or dispatches: the output tile (*tile_rows x *tile_cols of the
+ * output as stored) and the number of contraction splits (*splits, 1 when
+ * not split) that the entry points use when given a workspace of the size
+ * their query returns (with ws = NULL nothing is split).  layout:
+ *   ENC_LAYOUT_FWD    the forward projections: output [M, N] = X[M, K] W^T
+ *   ENC_LAYOUT_DGRAD  the input gradients: output [M, N] = dY[M, K] W[K, N]
+ *   ENC_LAYOUT_WGRAD  the weight gradients: dW[N, K] over M tokens (M, N, K
+ *                     as enc_linear_bwd_weight)
+ * Sizes follow the entry points' rules (ENC_ERR_INVALID / ENC_ERR_UNSUPPORTED
+ * as they would return); ENC_ERR_INVALID for another layout or a NULL
+ * output.  Host only: touches no device. */
+enum { ENC_LAYOUT_FWD = 0, ENC_LAYOUT_DGRAD = 1, ENC_LAYOUT_WGRAD = 2 };
+int enc_linear_plan(int layout, int M, int N, int K, int *tile_rows, int *tile_cols, int *splits);
+
 #ifdef __cplusplus
 }
 #endif

@@ -87,6 +87,7 @@ _SIGS = {
     "enc_oproj_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _sz, _p],
     "enc_qkv_bwd_data": [_i, _i, _i, _p, _p, _p, _p, _sz, _p],
     "enc_linear_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
+    "enc_linear_plan": [_i, _i, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)],
     "enc_linear_bwd_weight_workspace_bytes": [_i, _i, _i, ctypes.POINTER(_sz)],
     "enc_linear_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
     "enc_mlp_down_bwd_weight": [_i, _i, _i, _p, _p, _p, _p, _i, _p, _sz, _p],
@@ -417,6 +418,17 @@ def linear_workspace_bytes(M, N, K):
     n = _sz()
     _call("enc_linear_workspace_bytes", M, N, K, ctypes.byref(n))
     return n.value
+
+
+LAYOUT_FWD, LAYOUT_DGRAD, LAYOUT_WGRAD = 0, 1, 2
+
+
+def linear_plan(layout, M, N, K):
+    """(tile_rows, tile_cols, splits) of one projection product as the entry
+    points launch it with a workspace (host query, no device work)."""
+    r, c, sp = _i(), _i(), _i()
+    _call("enc_linear_plan", layout, M, N, K, ctypes.byref(r), ctypes.byref(c), ctypes.byref(sp))
+    return r.value, c.value, sp.value
 
 
 def _gemm_ws(M, N, K, ws, split, device):

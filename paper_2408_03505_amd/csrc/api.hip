@@ -650,6 +650,34 @@ int enc_linear_bwd_weight_workspace_bytes(int M, int N, int K, size_t *bytes) {
   return ok();
 }
 
+int enc_linear_plan(int layout, int M, int N, int K, int *tile_rows, int *tile_cols, int *splits) {
+  const char *fn = "enc_linear_plan";
+  if (layout != ENC_LAYOUT_FWD && layout != ENC_LAYOUT_DGRAD && layout != ENC_LAYOUT_WGRAD)
+    return fail(ENC_ERR_INVALID, "%s: unknown layout %d", fn, layout);
+  int r = linear_dims(fn, M, {N, K});
+  if (r) return r;
+  if (layout == ENC_LAYOUT_WGRAD && static_cast<long>(N) * K >= kMaxElems)
+    return fail(ENC_ERR_UNSUPPORTED, "%s: dW exceeds 2^31 elements", fn);
+  if (!tile_rows || !tile_cols || !splits) return fail(ENC_ERR_INVALID, "%s: an output pointer is NULL", fn);
+  // the GemmArgs geometry the launch helpers above build for each layout
+  GemmArgs a{};
+  bool AT = false, BT = false;
+  if (layout == ENC_LAYOUT_FWD) {
+    a.M = M, a.N = N, a.K = K, a.lda = K, a.ldb = K;
+  } else if (layout == ENC_LAYOUT_DGRAD) {
+    a.M = M, a.N = N, a.K = K, a.lda = K, a.ldb = N;
+    BT = true;
+  } else {
+    a.M = N, a.N = K, a.K = M, a.lda = N, a.ldb = K;
+    AT = BT = true;
+  }
+  const GemmPlan pl = gemm_plan(a.M, a.N, a.K, a.lda, a.ldb, AT, BT);
+  *tile_rows = pl.tile.bm;
+  *tile_cols = pl.tile.bn;
+  *splits = pl.splits;
+  return ok();
+}
+
 int enc_linear_bwd_weight(int M, int N, int K, const enc_bf16 *dY, const enc_bf16 *X, float *dW, float *db,
                           int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream) {
   const char *fn = "enc_linear_bwd_weight";

@@ -1035,8 +1035,7 @@ bool launch_cfg(const GemmArgs &a, hipStream_t s) {
 // least two waves of such tiles on 256 CUs; else 128x128 (4 waves of 64x64).
 template <bool AT, bool BT, Epi EPI>
 bool launch_any(const GemmArgs &a, hipStream_t s) {
-  const long big = static_cast<long>((a.M + 255) / 256) * ((a.N + 127) / 128);
-  if (big >= 512) return launch_cfg<256, 128, 64, 2, 2, AT, BT, EPI>(a, s);
+  if (any_tile(a.M, a.N).bm == 256) return launch_cfg<256, 128, 64, 2, 2, AT, BT, EPI>(a, s);
   return launch_cfg<128, 128, 64, 2, 2, AT, BT, EPI>(a, s);
 }
 
@@ -1213,14 +1212,10 @@ bool launch_pp_cfg(const GemmArgs &a, uint32_t a_bytes, uint32_t b_bytes, hipStr
 template <bool AT, bool BT, Epi EPI>
 bool launch_lds(const GemmArgs &a, hipStream_t s, TileShape t) {
   constexpr int BK = 64;
-  if ((!AT || !BT) && a.K % BK != 0) return false;  // contiguous-k operands need whole k-steps
-  // operand tensor extents (bytes) bound the buffer loads; keep every offset < 2^32
-  const uint64_t a_rows = AT ? static_cast<uint64_t>(a.K) : static_cast<uint64_t>(a.M);
-  const uint64_t b_rows = BT ? static_cast<uint64_t>(a.K) : static_cast<uint64_t>(a.N);
-  const uint64_t a_bytes = a_rows * a.lda * 2, b_bytes = b_rows * a.ldb * 2;
-  const uint64_t lim = (1ull << 32) - 1;
-  if (a_bytes + 600ull * a.lda * 2 > lim || b_bytes + 600ull * a.ldb * 2 > lim) return false;
-  const uint32_t ab = static_cast<uint32_t>(a_bytes), bb = static_cast<uint32_t>(b_bytes);
+  if (!lds_fits(a.M, a.N, a.K, a.lda, a.ldb, AT, BT)) return false;
+  // operand extents (bytes) bound the buffer loads
+  const uint32_t ab = static_cast<uint32_t>(static_cast<uint64_t>(AT ? a.K : a.M) * a.lda * 2);
+  const uint32_t bb = static_cast<uint32_t>(static_cast<uint64_t>(BT ? a.K : a.N) * a.ldb * 2);
   if (t.bm == 256 && t.bn == 256) {
     if constexpr (BT) return launch_pp_cfg<256, 256, 32, 2, 4, 4, AT, BT, EPI>(a, ab, bb, s);
     return launch_lds_cfg<256, 256, BK, 2, 4, 2, AT, BT, EPI>(a, ab, bb, s);

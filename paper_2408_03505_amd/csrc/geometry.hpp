@@ -147,6 +147,45 @@ inline SplitPlan gemm_split_plan(int M, int N, int K) {
   return {1, K, choose_tile(M, N, false)};
 }
 
+// Whether the direct-to-LDS kernels take a product (operands A(m, k) and
+// B(n, k) with leading dimensions lda, ldb; AT / BT: stored k-major):
+// contiguous-k operands need whole 64-wide k-steps, and the operand extents
+// that bound the buffer loads keep every offset below 2^32.  The others run
+// the register-staged kernel.
+inline bool lds_fits(int M, int N, int K, int lda, int ldb, bool AT, bool BT) {
+  if ((!AT || !BT) && K % 64 != 0) return false;
+  const unsigned long long lim = (1ull << 32) - 1;
+  const unsigned long long a_bytes = static_cast<unsigned long long>(AT ? K : M) * lda * 2;
+  const unsigned long long b_bytes = static_cast<unsigned long long>(BT ? K : N) * ldb * 2;
+  return a_bytes + 600ull * lda * 2 <= lim && b_bytes + 600ull * ldb * 2 <= lim;
+}
+
+// Tile of the register-staged kernel: 256x128 once that grid has 512 tiles,
+// else 128x128.
+inline TileShape any_tile(int M, int N) {
+  const long big = static_cast<long>((M + 255) / 256) * ((N + 127) / 128);
+  return big >= 512 ? TileShape{256, 128} : TileShape{128, 128};
+}
+
+// Output tile and contraction splits of a product as the launchers take it
+// when given a workspace of the queried size (forward: AT = BT = false;
+// input gradient: BT; weight gradient: AT and BT, M output rows, N output
+// columns, K tokens).
+struct GemmPlan {
+  TileShape tile;
+  int splits;
+};
+
+inline GemmPlan gemm_plan(int M, int N, int K, int lda, int ldb, bool AT, bool BT) {
+  const bool wgrad = AT && BT;
+  const bool fits = lds_fits(M, N, K, lda, ldb, AT, BT);
+  const SplitPlan sp = wgrad ? wgrad_split_plan(M, N, K) : gemm_split_plan(M, N, K);
+  const bool split_ok = wgrad ? M % 4 == 0 && N % 4 == 0 : N % 8 == 0;
+  if (sp.splits > 1 && split_ok && fits) return {sp.tile, sp.splits};
+  if (fits) return {choose_tile(M, N, wgrad), 1};
+  return {any_tile(M, N), 1};
+}
+
 inline size_t ws_round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 // Workspace of a split forward or input-gradient product: the fp32 partials

@@ -45,10 +45,10 @@ struct GemmArgs {
   float *Wf;           // fp32 output [M, ldy]
   float *db;           // fused row sums of A over k (fp32, [M]) for the weight gradient
   int accumulate;
-  // Split contraction (weight gradients only): when splits > 1, workgroup
-  // split s of a tile covers k in [s * k_chunk, min(K, (s + 1) * k_chunk))
-  // (k_chunk a multiple of the k-step) and writes its fp32 partial to
-  // Wf + s * split_stride and db + s * M, overwriting.
+  // Split contraction: when splits > 1, workgroup split s of a tile covers
+  // k in [s * k_chunk, min(K, (s + 1) * k_chunk)) (k_chunk a multiple of the
+  // k-step) and writes its fp32 partial to Wf + s * split_stride (and, for a
+  // weight gradient, db + s * M), overwriting.
   int splits;
   int k_chunk;
   size_t split_stride;

@@ -104,3 +104,12 @@ def test_per_kernel_entry_points_run():
             P if cls else S0, ws, S0)
     _ok("enc_calib_mfma", 4, 10, P, S0)
     _ok("enc_calib_copy", P, ctypes.c_void_p(0x10000 + (1 << 20)), 4096, S0)
+
+
+def test_linear_plan_queries():
+    r, c, sp = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    for layout in (B.LAYOUT_FWD, B.LAYOUT_DGRAD, B.LAYOUT_WGRAD):
+        for M, N, K in ((2048, 24576, 6144), (6304, 768, 768), (300, 200, 200), (1, 8, 8), (8192, 8192, 8200)):
+            _ok("enc_linear_plan", layout, M, N, K, ctypes.byref(r), ctypes.byref(c), ctypes.byref(sp))
+            assert r.value in (128, 256) and c.value in (128, 192, 256) and 1 <= sp.value <= 16
+    assert L.enc_linear_plan(9, 16, 8, 8, ctypes.byref(r), ctypes.byref(c), ctypes.byref(sp)) == B.ENC_ERR_INVALID

@@ -193,3 +193,30 @@ def test_cpu_baseline_reports_host_and_per_config_figures():
     assert set(r["per_config"]) == {"vit_tiny", "vit_base"} and set(r["single_thread"]) == {"vit_tiny", "vit_base"}
     for v in list(r["per_config"].values()) + list(r["single_thread"].values()):
         assert v["tflops"] > 0 and v["s_per_sequence"] > 0
+
+
+@pytest.mark.parametrize("tm,tn", [(8, 96), (8, 72), (16, 18), (9, 5), (1, 1), (24, 32)])
+def test_tile_order_model_covers_every_tile_once(tm, tn):
+    nb = tm * tn
+    seen = [bench._tile_of(p, nb, tm, tn) for p in range(nb)]
+    assert sorted(seen) == [(a, b) for a in range(tm) for b in range(tn)]
+
+
+@pytest.mark.parametrize("tm,tn,S", [(16, 6, 5), (3, 12, 7), (10, 10, 4)])
+def test_split_order_model_covers_every_item_once(tm, tn, S):
+    nb = tm * tn * S
+    seen = [bench._split_item(p, nb, tm, tn) for p in range(nb)]
+    assert sorted(seen) == [(s, a, b) for s in range(S) for a in range(tm) for b in range(tn)]
+
+
+def test_fetch_floor_bounds():
+    # ViT-22B MLP-up forward on 256x256 tiles: 8 x 96 tiles, three rounds; in
+    # a round each XCD runs 4 row tiles x 8 column tiles and fetches those
+    # 12 panels of 256 rows x 6144 bf16
+    assert bench.fetch_floor(2048, 24576, 6144, 256, 256, 1) == 8 * 3 * 12 * 256 * 6144 * 2
+    for rows, cols, K, bm, bn, sp in ((2048, 18432, 6144, 256, 192, 1), (6304, 768, 768, 128, 128, 1),
+                                      (768, 768, 6304, 128, 128, 12), (2000, 72 * 8, 1024, 128, 128, 1)):
+        f = bench.fetch_floor(rows, cols, K, bm, bn, sp)
+        once = 2 * K * (rows + cols)  # each operand fetched once
+        tiles = -(-rows // bm) * -(-cols // bn)
+        assert once <= f <= tiles * sp * 2 * (bm + bn) * -(-K // sp), (rows, cols, K)

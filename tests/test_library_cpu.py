@@ -106,6 +106,52 @@ def test_weight_gradient_split_plan_sizes():
     assert wg > 0 and B.layer_workspace_bytes(base) >= wg
 
 
+def test_linear_plan_matches_the_workspace_queries():
+    # a plan splits exactly when the workspace query asks for partials, and
+    # the workspace holds one fp32 partial per split
+    r256 = lambda x: (x + 255) // 256 * 256
+    for M, N, K in ((2048, 768, 6144), (2048, 24576, 6144), (1000, 2048, 512), (300, 200, 1280),
+                    (2048, 2304, 6144), (6304, 768, 3072)):
+        for layout in (B.LAYOUT_FWD, B.LAYOUT_DGRAD):
+            bm, bn, sp = B.linear_plan(layout, M, N, K)
+            ws = B.linear_workspace_bytes(M, N, K)
+            assert (sp > 1) == (ws > 0), (M, N, K, layout)
+            if sp > 1:
+                assert ws == r256(sp * M * N * 4) and (bm, bn) == (128, 128)
+    for M, N, K in ((6304, 768, 768), (6304, 3072, 768), (4112, 1280, 1280), (2048, 24576, 6144),
+                    (2048, 6144, 768), (2000, 768, 256)):
+        bm, bn, sp = B.linear_plan(B.LAYOUT_WGRAD, M, N, K)
+        ws = B.linear_bwd_weight_workspace_bytes(M, N, K)
+        assert (sp > 1) == (ws > 0), (M, N, K)
+        if sp > 1:
+            assert ws == r256(sp * N * K * 4) + r256(sp * N * 4)
+            # every split covers at least 512 tokens but the last
+            assert (M + sp - 1) // sp >= 512
+
+
+def test_linear_plan_tiles():
+    # ViT-22B layer (2048 tokens): 256x256 tiles where the grid fills whole
+    # rounds of the 256 CUs, 256x192 where 256x256 would leave CUs idle
+    assert B.linear_plan(B.LAYOUT_FWD, 2048, 24576, 6144) == (256, 256, 1)
+    assert B.linear_plan(B.LAYOUT_FWD, 2048, 18432, 6144) == (256, 192, 1)
+    assert B.linear_plan(B.LAYOUT_DGRAD, 2048, 6144, 24576) == (256, 192, 1)
+    assert B.linear_plan(B.LAYOUT_WGRAD, 2048, 24576, 6144) == (256, 256, 1)
+    assert B.linear_plan(B.LAYOUT_WGRAD, 2048, 6144, 24576) == (256, 256, 1)
+    # a contiguous contraction that is not a multiple of 64 takes the
+    # register-staged kernel's tiles, unsplit
+    assert B.linear_plan(B.LAYOUT_FWD, 300, 200, 200) == (128, 128, 1)
+    assert B.linear_plan(B.LAYOUT_FWD, 8192, 8192, 8200) == (256, 128, 1)
+    # arguments are checked like the entry points'
+    for args, code in (((7, 2048, 768, 768), B.ENC_ERR_INVALID), ((B.LAYOUT_FWD, 0, 768, 768), B.ENC_ERR_INVALID),
+                       ((B.LAYOUT_FWD, 16, 770, 768), B.ENC_ERR_UNSUPPORTED)):
+        with pytest.raises(B.EncError) as e:
+            B.linear_plan(*args)
+        assert e.value.status == code
+    L = B.lib()
+    i = ctypes.c_int()
+    assert L.enc_linear_plan(B.LAYOUT_FWD, 16, 64, 64, None, ctypes.byref(i), ctypes.byref(i)) == B.ENC_ERR_INVALID
+
+
 def test_workspace_sizes():
     assert B.layer_workspace_bytes(VIT22B) > 0
     for rows, cols in ((2048, 6144), (10, 192), (6304, 768), (1, 8)):
