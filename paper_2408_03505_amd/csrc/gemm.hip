@@ -663,7 +663,6 @@ struct FragAddr {
 // reads have a whole k-step of MFMA work to land in.
 template <int NM, int NR, int M = 0>
 __device__ __forceinline__ void interleave_reads() {
-#ifndef OPTIMUS_NO_SCHED_GROUPS
   if constexpr (M < NM) {
     constexpr int per = (NR + NM - 1) / NM;
     constexpr int done = M * per < NR ? M * per : NR;
@@ -672,7 +671,6 @@ __device__ __forceinline__ void interleave_reads() {
     if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // then r LDS reads
     interleave_reads<NM, NR, M + 1>();
   }
-#endif
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int STAGES, bool AT, bool BT, Epi EPI>
@@ -850,11 +848,10 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_lds_kernel(GemmArgs p, ui
 // refilled two stages ahead, the other through two slots, one stage ahead.
 // A 256x192x64 tile uses 3 x 32 + 2 x 24 KB = 144 KB (a 256x256 one would
 // take all 160 KB).  Each stage issues the shallow operand's next stage
-// first and the deep operand's stage a sub-step later (kDeepSpread), so the
-// wait that ends the stage leaves exactly the latter in flight; one barrier
-// per stage as in the two-stage kernel.  A stage's refill then has two
-// stages of matrix work to land in instead of one.
-constexpr bool kDeepSpread = true;
+// first and the deep operand's stage a sub-step later, so the wait that ends
+// the stage leaves exactly the latter in flight; one barrier per stage as in
+// the two-stage kernel.  A stage's refill then has two stages of matrix work
+// to land in instead of one.
 
 template <int BM, int BN, int BK, int WM, int WN, bool A_DEEP, bool BT, Epi EPI>
 __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_deep_kernel(GemmArgs p, uint32_t a_bytes, uint32_t b_bytes) {
@@ -940,14 +937,13 @@ __global__ __launch_bounds__(WM *WN * 64, 1) void gemm_deep_kernel(GemmArgs p, u
     // refill the slots stage t-1 used (every wave finished reading them
     // before the barrier that ended stage t-1): shallow operand first
     if (t + 1 < nk) issue_shallow(t + 1);
-    if (!kDeepSpread && t + 2 < nk) issue_deep(t + 2);
     const lds_char *As = a_stage(t), *Bs = b_stage(t);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int c = kk & 1, n = c ^ 1;
       // the deep operand has two stages of lead: its refill can go out a
       // sub-step after the shallow one's
-      if (kDeepSpread && kk == 1 && t + 2 < nk) issue_deep(t + 2);
+      if (kk == 1 && t + 2 < nk) issue_deep(t + 2);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll

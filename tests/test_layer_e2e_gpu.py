@@ -34,13 +34,13 @@ SAVED = ("y1", "mean1", "rstd1", "qkv", "o", "lse", "h", "y2", "mean2", "rstd2",
 
 
 def _record(name, errs, gerrs):
-    """Append the measured errors to gpurun_out/parity_e2e.jsonl when that
-    folder exists (a GPU run's output folder); otherwise only print them."""
+    """Print the measured errors, and append them as one JSON line to the
+    file OPTIMUS_PARITY_LOG names, if set."""
     line = {"config": name, "act": errs, "grad": gerrs}
     print("[parity-e2e] " + json.dumps(line), flush=True)
-    out = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
-    if os.path.isdir(out):
-        with open(os.path.join(out, "parity_e2e.jsonl"), "a") as f:
+    path = os.environ.get("OPTIMUS_PARITY_LOG")
+    if path:
+        with open(path, "a") as f:
             f.write(json.dumps(line) + "\n")
 
 
