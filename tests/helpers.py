@@ -29,3 +29,29 @@ def cuda(t):
 def announce(msg):
     """Print (and flush) what the next GPU step runs, so a failure is named."""
     print(f"[gpu-case] {msg}", flush=True)
+
+
+GUARD = 4096  # elements of guard band after every output
+
+
+def guarded(shape, dtype):
+    """An output tensor followed by a guard band filled with a sentinel."""
+    n = int(np.prod(shape))
+    buf = torch.empty(n + GUARD, dtype=dtype, device="cuda")
+    if dtype == torch.bfloat16:
+        buf.view(torch.int16).fill_(0x7FA5)  # a NaN payload no kernel writes
+    else:
+        buf.view(torch.int32).fill_(0x7FC0DEAD)
+    return buf[:n].view(shape), buf
+
+
+def guard_intact(buf, n):
+    tail = buf[n:]
+    if buf.dtype == torch.bfloat16:
+        return bool((tail.view(torch.int16) == 0x7FA5).all())
+    return bool((tail.view(torch.int32) == 0x7FC0DEAD).all())
+
+
+def exact_equal(got, want):
+    g = f64(got)
+    return bool(np.array_equal(g, want)), float(np.abs(g - want).max())

@@ -13,38 +13,12 @@ import pytest
 import torch
 
 import oracle
-from helpers import TOL_ACT, TOL_GRAD, announce, cuda, f64, max_rel
+from helpers import TOL_ACT, TOL_GRAD, announce, cuda, exact_equal, f64, guard_intact, guarded, max_rel
 from paper_2408_03505_amd import binding as B
 from paper_2408_03505_amd.synthetic import random_bf16, random_int_bf16, random_sparse_sign_bf16
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
-
-GUARD = 4096  # elements of guard band after every output
-
-
-def guarded(shape, dtype):
-    """An output tensor followed by a guard band filled with a sentinel."""
-    n = int(np.prod(shape))
-    buf = torch.empty(n + GUARD, dtype=dtype, device="cuda")
-    if dtype == torch.bfloat16:
-        buf.view(torch.int16).fill_(0x7FA5)  # a NaN payload no kernel writes
-    else:
-        buf.view(torch.int32).fill_(0x7FC0DEAD)
-    return buf[:n].view(shape), buf
-
-
-def guard_intact(buf, n):
-    tail = buf[n:]
-    if buf.dtype == torch.bfloat16:
-        return bool((tail.view(torch.int16) == 0x7FA5).all())
-    return bool((tail.view(torch.int32) == 0x7FC0DEAD).all())
-
-
-def exact_equal(got, want):
-    g = f64(got)
-    return bool(np.array_equal(g, want)), float(np.abs(g - want).max())
-
 
 # --------------------------------------------------------------------------- LayerNorm
 
