@@ -1,5 +1,5 @@
-"""Seeded random shapes through the three GEMM layouts (through the C ABI),
-bit-exact against the oracle.
+"""Seeded random shapes through the GEMM layouts, attention and LayerNorm
+(through the C ABI), against the oracle.
 
 Besides the hand-picked shapes of the per-kernel tests, these draw output
 and contraction sizes at random (feature widths multiples of 8, any token
@@ -7,7 +7,9 @@ count): general ones, small outputs with long contractions so that the
 library's split plans run, and grids large enough for 256-row tiles.  Inputs are small integers (sparse signs for the
 bf16-output products) so that fp32 accumulation and bf16 rounding are
 exact: every product must equal the oracle bit for bit, with and without a
-workspace, and leave the guard band after each output untouched.
+workspace, and leave the guard band after each output untouched.  Attention
+and LayerNorm draw sequence lengths, head counts, head dims, row counts and
+widths at random and meet the parity bar of the per-kernel tests.
 """
 
 import numpy as np
@@ -15,9 +17,9 @@ import pytest
 import torch
 
 import oracle
-from helpers import announce, cuda, exact_equal, f64, guard_intact, guarded
+from helpers import TOL_ACT, TOL_GRAD, announce, cuda, exact_equal, f64, guard_intact, guarded, max_rel
 from paper_2408_03505_amd import binding as B
-from paper_2408_03505_amd.synthetic import random_int_bf16, random_sparse_sign_bf16
+from paper_2408_03505_amd.synthetic import random_bf16, random_int_bf16, random_sparse_sign_bf16
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -39,10 +41,17 @@ def _shapes():
         wg.append((int(rng.integers(1024, 3001)), 8 * int(rng.integers(1, 97)), 8 * int(rng.integers(1, 97))))
     for _ in range(3):
         wg.append((int(rng.integers(500, 2049)), 8 * int(rng.integers(300, 513)), 8 * int(rng.integers(300, 513))))
-    return mk, wg
+    at = []  # attention (batch, seq, heads, head_dim)
+    for hi in (701, 701, 701, 701, 701, 100, 100, 100):
+        at.append((int(rng.integers(1, 5)), int(rng.integers(1, hi)), int(rng.integers(1, 7)),
+                   int(rng.choice([64, 80, 128]))))
+    for _ in range(2):  # grids above 256 workgroups
+        at.append((8, int(rng.integers(100, 401)), 16, int(rng.choice([64, 80, 128]))))
+    ln = [(int(rng.integers(1, hi)), 8 * int(rng.integers(1, 1025))) for hi in (5001,) * 7 + (40,) * 3]
+    return mk, wg, at, ln
 
 
-MK, WG = _shapes()
+MK, WG, AT, LN = _shapes()
 
 
 def _density(K):
@@ -88,3 +97,52 @@ def test_random_weight_gradient(M, N, K):
         ok, err = exact_equal(db, rdb)
         assert ok, ("db", split, err)
         assert guard_intact(wbuf, N * K) and guard_intact(bbuf, N)
+
+
+@pytest.mark.parametrize("Bn,S,nh,d", AT)
+def test_random_attention(Bn, S, nh, d):
+    announce(f"random attention B={Bn} S={S} heads={nh} d={d}")
+    qkv = random_bf16((Bn * S, 3 * nh * d), 321, 1.5)
+    dO = random_bf16((Bn * S, nh * d), 322)
+    o, obuf = guarded((Bn * S, nh * d), torch.bfloat16)
+    lse, lbuf = guarded((Bn, nh, S), torch.float32)
+    B.enc_attn_fwd(Bn, S, nh, d, cuda(qkv), o=o, lse=lse)
+    dqkv, dbuf = guarded((Bn * S, 3 * nh * d), torch.bfloat16)
+    B.enc_attn_bwd(Bn, S, nh, d, cuda(qkv), o, lse, cuda(dO), dqkv=dqkv)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention_fwd(f64(qkv), Bn, S, nh, d)
+    assert max_rel(f64(o), ro) < TOL_ACT
+    assert np.abs(f64(lse) - rl).max() < 2e-3 * max(1.0, np.abs(rl).max())
+    ref = oracle.attention_bwd(f64(qkv), f64(dO), Bn, S, nh, d)
+    got, A = f64(dqkv), nh * d
+    for part, sl in (("dq", slice(0, A)), ("dk", slice(A, 2 * A)), ("dv", slice(2 * A, 3 * A))):
+        assert max_rel(got[:, sl], ref[:, sl]) < TOL_GRAD, part
+    assert guard_intact(obuf, o.numel()) and guard_intact(lbuf, lse.numel()) and guard_intact(dbuf, dqkv.numel())
+
+
+@pytest.mark.parametrize("rows,cols", LN)
+def test_random_layernorm(rows, cols):
+    announce(f"random layernorm rows={rows} cols={cols}")
+    x = (random_bf16((rows, cols), 331, 1.5).float() + 0.4).to(torch.bfloat16)
+    g = (1 + random_bf16((cols,), 332, 0.2).float()).to(torch.bfloat16)
+    b = random_bf16((cols,), 333, 0.2)
+    dy, dres = random_bf16((rows, cols), 334), random_bf16((rows, cols), 335)
+    y, ybuf = guarded((rows, cols), torch.bfloat16)
+    mean, mbuf = guarded((rows,), torch.float32)
+    rstd, rbuf = guarded((rows,), torch.float32)
+    B.enc_ln_fwd(cuda(x), cuda(g), cuda(b), 1e-6, y=y, mean=mean, rstd=rstd)
+    dx, dxbuf = guarded((rows, cols), torch.bfloat16)
+    dg, dgbuf = guarded((cols,), torch.float32)
+    db, dbbuf = guarded((cols,), torch.float32)
+    B.enc_ln_bwd(cuda(dy), cuda(x), mean, rstd, cuda(g), dresid=cuda(dres), dx=dx, dgamma=dg, dbeta=db)
+    torch.cuda.synchronize()
+    ry, rm, rr = oracle.layernorm_fwd(f64(x), f64(g), f64(b), 1e-6)
+    assert max_rel(f64(y), ry) < TOL_ACT
+    assert np.abs(f64(mean) - rm).max() < 1e-5 * max(1.0, np.abs(rm).max())
+    assert np.abs(f64(rstd) / rr - 1).max() < 1e-5
+    rdx, rdg, rdb = oracle.layernorm_bwd(f64(dy), f64(x), rm, rr, f64(g))
+    assert max_rel(f64(dx), rdx + f64(dres)) < TOL_GRAD
+    assert max_rel(f64(dg), rdg) < TOL_GRAD and max_rel(f64(db), rdb) < TOL_GRAD
+    for buf, n in ((ybuf, rows * cols), (mbuf, rows), (rbuf, rows), (dxbuf, rows * cols), (dgbuf, cols),
+                   (dbbuf, cols)):
+        assert guard_intact(buf, n)
