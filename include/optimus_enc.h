@@ -118,7 +118,9 @@ int enc_abi_version(void);
 
 /* ------------------------------------------------------------ sizing */
 
-/* Validates cfg and fills the saved-buffer layout. */
+/* [Caller-owned buffers of one scheduling unit: the layer's saved tensors
+ * and workspaces (§4.2; memory accounting §4.5)]
+ * Validates cfg and fills the saved-buffer layout. */
 int enc_saved_layout(const enc_cfg_t *cfg, enc_saved_layout_t *layout);
 /* Workspace bytes that encoder_layer_fwd / encoder_layer_bwd need. */
 int enc_layer_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes);
@@ -387,20 +389,23 @@ typedef struct {
   size_t total;
 } enc_psaved_layout_t;
 
-/* Fills layout with the offsets above for cfg (256-byte aligned, disjoint);
+/* [ViT-22B block (Appendix A): buffers]
+ * Fills layout with the offsets above for cfg (256-byte aligned, disjoint);
  * ENC_ERR_INVALID / ENC_ERR_UNSUPPORTED for a bad cfg. */
 int enc_parallel_saved_layout(const enc_cfg_t *cfg, enc_psaved_layout_t *layout);
 /* Workspace bytes encoder_parallel_bwd needs. */
 int enc_parallel_workspace_bytes(const enc_cfg_t *cfg, size_t *bytes);
 
-/* Forward of the block: LN, QKV projection, QK norm, attention, output
+/* [ViT-22B block (Appendix A): forward as one scheduling unit (§4.2)]
+ * Forward of the block: LN, QKV projection, QK norm, attention, output
  * projection + residual, MLP up + GELU (from y), MLP down + residual, on one
  * stream.  x, out: [M, H]; saved: enc_parallel_saved_layout().total bytes. */
 int encoder_parallel_fwd(const enc_cfg_t *cfg, const enc_pparams_t *params,
                          const enc_bf16 *x, enc_bf16 *out, void *saved,
                          enc_stream_t stream);
 
-/* (The block's two composites run every product unsplit.)
+/* [ViT-22B block (Appendix A): backward as one scheduling unit (§4.2)]
+ * (The block's two composites run every product unsplit.)
  * Exact gradient of encoder_parallel_fwd.  dy of the shared LayerNorm is the
  * sum of both branches' input gradients (the QKV input gradient adds the
  * MLP branch's in its epilogue); dx = dout + LN backward(dy).  accumulate as
@@ -411,7 +416,8 @@ int encoder_parallel_bwd(const enc_cfg_t *cfg, const enc_pparams_t *params,
                          const enc_pgrads_t *grads, int accumulate, void *ws,
                          size_t ws_bytes, enc_stream_t stream);
 
-/* QK normalisation: qkvn = qkv with every (token, head) query vector replaced
+/* [ViT-22B block step (Appendix A): query/key normalisation]
+ * QK normalisation: qkvn = qkv with every (token, head) query vector replaced
  * by LN(q) * qn_g + qn_b and every key vector by LN(k) * kn_g + kn_b (LN over
  * head_dim, biased variance, eps inside the square root); values copied.
  * qkv, qkvn: [M, 3*heads*head_dim]; stats: [M, heads, 4] fp32 (query mean,
@@ -421,7 +427,8 @@ int enc_qk_norm_fwd(int M, int heads, int head_dim, const enc_bf16 *qkv,
                     const enc_bf16 *kn_g, const enc_bf16 *kn_b, float eps,
                     enc_bf16 *qkvn, float *stats, enc_stream_t stream);
 
-/* Workspace bytes enc_qk_norm_bwd needs (per-block partial sums of the four
+/* [ViT-22B block step (Appendix A): backward of the query/key normalisation]
+ * Workspace bytes enc_qk_norm_bwd needs (per-block partial sums of the four
  * affine gradients, reduced in a fixed order). */
 int enc_qk_norm_bwd_workspace_bytes(int M, int heads, int head_dim, size_t *bytes);
 
@@ -436,7 +443,8 @@ int enc_qk_norm_bwd(int M, int heads, int head_dim, const enc_bf16 *dqkvn,
                     int accumulate, void *ws, size_t ws_bytes,
                     enc_stream_t stream);
 
-/* QKV input gradient plus an addend (the other branch's input gradient of
+/* [ViT-22B block step (Appendix A): the shared LayerNorm's input gradient]
+ * QKV input gradient plus an addend (the other branch's input gradient of
  * the shared LayerNorm output): dy[M, H] = dqkv[M, 3A] * w_qkv[3A, H] +
  * addend[M, H], accumulated in fp32 before one rounding to bf16. */
 int enc_qkv_bwd_data_add(int M, int H, int A, const enc_bf16 *dqkv,
@@ -468,7 +476,8 @@ int enc_patch_embed_fwd(int batch, int channels, int img_h, int img_w, int patch
                         const enc_bf16 *images, const enc_bf16 *w_pe, const enc_bf16 *b_pe, const enc_bf16 *cls,
                         const enc_bf16 *pos, enc_bf16 *patches, enc_bf16 *x0, void *ws, size_t ws_bytes,
                         enc_stream_t stream);
-/* Parameter gradients of the patch embedding from dx0 [B*S, hidden] and the
+/* [Whole ViT encoder (Appendix A): backward of the patch embedding]
+ * Parameter gradients of the patch embedding from dx0 [B*S, hidden] and the
  * forward's patches: dw_pe [hidden, Kp], db_pe [hidden], dpos [S, hidden]
  * (sum over the batch in order), dcls [hidden] (only with has_cls) -- all
  * fp32, overwritten or (accumulate=1) added.  The images get no gradient.
@@ -477,7 +486,8 @@ int enc_patch_embed_bwd(int batch, int channels, int img_h, int img_w, int patch
                         const enc_bf16 *dx0, const enc_bf16 *patches, float *dw_pe, float *db_pe, float *dcls,
                         float *dpos, int accumulate, void *ws, size_t ws_bytes, enc_stream_t stream);
 
-/* A stack of `layers` sequential encoder layers (params[layers], each as for
+/* [Whole ViT encoder (Appendix A): the layer stack and final LayerNorm]
+ * A stack of `layers` sequential encoder layers (params[layers], each as for
  * encoder_layer_fwd) followed by a final LayerNorm (lnf_g, lnf_b):
  * out = LN(layer_{L-1}(... layer_0(x0))).  saved (enc_stack_saved_bytes)
  * holds every layer's output (the next layer's input), every layer's saved
@@ -487,7 +497,8 @@ int enc_stack_workspace_bytes(const enc_cfg_t *cfg, int layers, size_t *bytes);
 int encoder_stack_fwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params,
                       const enc_bf16 *lnf_g, const enc_bf16 *lnf_b, const enc_bf16 *x0,
                       enc_bf16 *out, void *saved, enc_stream_t stream);
-/* Backward of encoder_stack_fwd: dx0 and the gradients of every layer
+/* [Whole ViT encoder (Appendix A): backward of the stack]
+ * Backward of encoder_stack_fwd: dx0 and the gradients of every layer
  * (grads[layers]) and of the final LayerNorm; accumulate as for
  * encoder_layer_bwd.  ws: enc_stack_workspace_bytes. */
 int encoder_stack_bwd(const enc_cfg_t *cfg, int layers, const enc_params_t *params,
